@@ -1,0 +1,15 @@
+"""CPU oracle for the fused W4A16 / W8A16 matmul.
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
+benchmark's CPU-baseline leg, never by the library.
+"""
+from .awq_oracle import (  # noqa: F401
+    dequant,
+    dequant_f16,
+    group_of,
+    matmul,
+    to_f16,
+    unpack_w4,
+    w4a16,
+    w8a16,
+)
