@@ -1,0 +1,198 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused W4A16 matmul on one MI355X.
+
+One step = one pass of the hot path over the Llama-3-8B MLP shapes, synthetic
+seeded data (weights pre-packed offline, inputs resident in HBM):
+  * prefill GEMM  M=2048, K=4096,  N=14336, group 128  (up-projection shape)
+  * prefill GEMM  M=2048, K=14336, N=4096,  group 128  (down-projection shape)
+  * decode GEMV   M=1,    K=4096,  N=14336, group 128, repeated over
+    GEMV_REPS distinct weight copies (one token through GEMV_REPS layers), so
+    every GEMV streams its weights from HBM, not from the 256 MB MALL.
+
+Prints ONE JSON line.  `value` is the prefill GEMM throughput in TFLOP/s
+(2*M*N*K per GEMM over the GEMM kernels' time); the decode GEMV's effective
+HBM bandwidth (packed codes + fp16 scales + zero-points per launch over its
+average launch time) is reported beside it, each with its roofline fraction.
+Kernel times come from HIP events recorded on the launch stream.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+GEMM_SHAPES = [(2048, 4096, 14336), (2048, 14336, 4096)]
+GEMV_SHAPE = (1, 4096, 14336)
+GROUP = 128
+GEMV_REPS = 32
+PEAK_F16_TFLOPS = 2516.6      # 256 CU x 4096 FLOP/clk x 2.4 GHz (dense fp16 MFMA)
+PEAK_HBM_GBS = 8000.0
+
+
+def algo_bytes_w4(K, N, G=GROUP):
+    """Bytes the method must move per launch: packed 4-bit codes, fp16 scales
+    and 4-bit zero-points (the AWQ storage), activations and output excluded."""
+    return K * N // 2 + (K // G) * N * 2 + (K // G) * N // 2
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-cols", type=int, default=1024)
+    return ap.parse_args()
+
+
+def cpu_baseline(sample_cols):
+    """The oracle (fp64, numpy/BLAS) timed on the host on a bounded sample of
+    the prefill workload: all M=2048 rows, K=4096, the first `sample_cols`
+    output columns of the N=14336 weight."""
+    import oracle
+    from paper_2606_11357_amd.synth import make_inputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    M, K, N = GEMM_SHAPES[0]
+    d = make_inputs(4, M, K, sample_cols, seed=0)
+    t0 = time.perf_counter()
+    y = oracle.w4a16(d["x"], d["qweight"], d["qzeros"], d["s"], GROUP)
+    t = time.perf_counter() - t0
+    assert np.isfinite(y).all()
+    flops = 2.0 * M * K * sample_cols
+    return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle", "seconds": round(t, 3),
+            "sample": f"W4A16 oracle (unpack, fp64 dequant, fp64 matmul) at M={M}, K={K}, "
+                      f"first {sample_cols} of N={N} columns"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
+              "(nothing here runs across GPUs)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_11357_amd import tilefuse as tf
+    from paper_2606_11357_amd.synth import make_inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    tf.load()
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+
+    def upload(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    def packed_w4(d):
+        return tf.pack_w4(upload(d["qweight"]), upload(d["qzeros"]), upload(d["s"]),
+                          d["K"], d["N"], GROUP)
+
+    # ---- inputs (offline: generation + pack are outside the timed region)
+    gemm = []
+    for (M, K, N) in GEMM_SHAPES:
+        d = make_inputs(4, M, K, N, group=GROUP, seed=0)
+        p = packed_w4(d)
+        gemm.append(dict(M=M, K=K, N=N, A=upload(d["x"]), packed=p,
+                         out=torch.empty((M, N), dtype=torch.float16, device=dev)))
+        del d
+    M1, K1, N1 = GEMV_SHAPE
+    d = make_inputs(4, M1, K1, N1, group=GROUP, seed=0)
+    p0 = packed_w4(d)
+    gemv_copies = [p0] + [p0.clone() for _ in range(GEMV_REPS - 1)]
+    x1 = upload(d["x"])
+    y1 = torch.empty((M1, N1), dtype=torch.float16, device=dev)
+    del d
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        for g in gemm:
+            tf.w4a16_gemm(g["A"], g["packed"], g["K"], g["N"], GROUP, out=g["out"])
+        if ev is not None:
+            ev[1].record(stream)
+        for p in gemv_copies:
+            tf.w4a16_gemv(x1, p, K1, N1, GROUP, out=y1)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(events[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    gemm_ms = sum(e[0].elapsed_time(e[1]) for e in events) / args.steps
+    gemv_ms = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps
+    gemm_flops = sum(2.0 * g["M"] * g["N"] * g["K"] for g in gemm)
+    tflops = gemm_flops / (gemm_ms * 1e-3) / 1e12
+    gemv_us = gemv_ms * 1e3 / GEMV_REPS
+    gemv_bytes = algo_bytes_w4(K1, N1)
+    gemv_gbs = gemv_bytes / (gemv_us * 1e-6) / 1e9
+    gemm_us_each = [None, None]
+
+    line = {
+        "metric": "W4A16 GEMM TFLOP/s (M=2048) + GEMV eff. HBM GB/s (M=1), % of roofline",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": "W4A16 (AWQ-style, G=128) prefill GEMM M=2048 at (K=4096,N=14336) and "
+                        "(K=14336,N=4096) + decode GEMV M=1 K=4096 N=14336 x%d weight copies" % GEMV_REPS,
+            "group": GROUP,
+            "weights": "4-bit codes, fp16 scales, 4-bit zero-points (seeded uniform)",
+            "activations": "fp16 N(0,1)",
+        },
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(tflops, 2),
+            "peak": PEAK_F16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(tflops / PEAK_F16_TFLOPS, 4),
+            "traffic": None,
+            "kernel": "gemm_kernel<4> (both prefill shapes)",
+        },
+        "gemv": {
+            "value": round(gemv_gbs, 1),
+            "unit": "GB/s",
+            "us_per_launch": round(gemv_us, 3),
+            "bytes_per_launch": gemv_bytes,
+            "roofline": {"bound": "hbm", "achieved": round(gemv_gbs, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(gemv_gbs / PEAK_HBM_GBS, 4),
+                         "traffic": None, "kernel": "gemv_kernel<4,1>"},
+        },
+        "gemm_ms": round(gemm_ms, 4),
+    }
+    del gemm_us_each
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(args.cpu_sample_cols)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,149 @@
+/*
+ * tilefuse.h -- C ABI of the fused weight-only quantized matmul for gfx950.
+ *
+ * The operation (TileFuse, Sections 2.1-2.2 and 4.2-4.3):
+ *
+ *     C[m, n] = sum_k A[m, k] * w_hat[k, n],      C = A x B (Section 2.1)
+ *     w_hat[k, n] = s[g, n] * (q[k, n] - z[g, n]), g = floor(k / G)  (Eq. 2)
+ *
+ * A is fp16 [M, K] row-major, the weights are 4-bit (W4A16) or 8-bit (W8A16)
+ * integer codes with one fp16 scale and one integer zero-point per group of G
+ * consecutive k in one column n (Section 2.2), accumulation is fp32 and C is
+ * fp16 [M, N] row-major, rounded to nearest even.  The weights never exist in
+ * memory as fp16: each kernel unpacks and dequantizes them on the fly (Section
+ * 4.3, fused unpack -> dequantize -> multiply-accumulate).
+ *
+ * Weights are first rearranged once, offline, into a device-private layout
+ * (tf_pack_w4 / tf_pack_w8; the GPU counterpart of the offline pre-tiling of
+ * Section 4.2).  The packed buffer is opaque; pass the same (K, N, group) to
+ * the matmul calls that were given to the pack call.
+ *
+ * Conventions for every entry point:
+ *  - All array pointers are DEVICE pointers (hipMalloc / torch CUDA tensors).
+ *  - fp16 values travel as uint16_t bit patterns.
+ *  - `stream` is a hipStream_t passed as void*; NULL means the null stream.
+ *    Calls only enqueue work on `stream` and return; the caller synchronizes.
+ *  - The caller allocates and frees every buffer; the library keeps no device
+ *    memory and no mutable global state, so calls are thread-safe.
+ *  - Arguments are validated before any HIP call; a rejected call enqueues
+ *    nothing.  Only TF_ERR_HIP comes from the runtime (launch failure).
+ *  - Outputs must not overlap inputs.
+ *  - No C++ exception crosses this boundary; the library prints nothing.
+ */
+#ifndef TILEFUSE_H
+#define TILEFUSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes (returned as int; negative means failure). */
+enum tf_status {
+    TF_OK = 0,
+    TF_ERR_NULL = -1,   /* a required pointer is NULL                          */
+    TF_ERR_SHAPE = -2,  /* M < 1, K or N <= 0, K % group != 0, N % 8 != 0,
+                           or a dimension above TF_MAX_DIM                      */
+    TF_ERR_GROUP = -3,  /* group is not a positive multiple of 32              */
+    TF_ERR_ALIGN = -4,  /* a pointer is not 16-byte aligned                    */
+    TF_ERR_ARG = -5,    /* other bad argument: bits not 4/8, GEMV with M > 8,
+                           unknown dtype, workspace too small                  */
+    TF_ERR_HIP = -6     /* the HIP runtime reported an error at launch         */
+};
+
+/* Output dtypes of tf_dequant. */
+enum tf_dtype { TF_F16 = 1, TF_F32 = 2 };
+
+/* Largest accepted K and N (each) and M; keeps every byte offset in int64
+ * and every per-kernel index in 32 bits. */
+#define TF_MAX_DIM 65536
+#define TF_MAX_M (1 << 20)
+/* Largest M accepted by the GEMV entry points (decode, Section 2.1). */
+#define TF_GEMV_MAX_M 8
+
+/* Library version of the packed layout; bumps whenever the layout changes. */
+int tf_layout_version(void);
+
+/* Human-readable text for a status code (static storage, never NULL). */
+const char* tf_status_str(int status);
+
+/*
+ * Size in bytes of the packed buffer for a (bits, K, N, group) weight.
+ * bits is 4 or 8.  Returns > 0, or a negative tf_status on bad arguments.
+ */
+int64_t tf_packed_bytes(int bits, int64_t K, int64_t N, int group);
+
+/*
+ * Offline pre-tiling of a 4-bit AWQ weight (Section 4.2: weights are known at
+ * deployment, so the rearrangement is done once and is not on the timed path).
+ *   qweight  int32 [K, N/8]   nibble i (bits 4i..4i+3) of word j = q[k, 8j+i]
+ *   qzeros   int32 [K/G, N/8] same packing, z[g, 8j+i]
+ *   scales   fp16  [K/G, N]   s[g, n]
+ *   packed   tf_packed_bytes(4, K, N, group) bytes, written entirely
+ * Requires N % 8 == 0, group % 32 == 0, K % group == 0, 16-byte aligned
+ * pointers.  Integer rearrangement only: scales are copied bit for bit.
+ */
+int tf_pack_w4(const int32_t* qweight, const int32_t* qzeros, const uint16_t* scales,
+               int64_t K, int64_t N, int group, void* packed, void* stream);
+
+/*
+ * Offline pre-tiling of an 8-bit weight with per-group zero-points.
+ *   qweight  uint8 [K, N]     q[k, n]
+ *   zeros    uint8 [K/G, N]   z[g, n]
+ *   scales   fp16  [K/G, N]   s[g, n]
+ *   packed   tf_packed_bytes(8, K, N, group) bytes
+ * Same constraints as tf_pack_w4 (N % 8 == 0 keeps rows 8-byte aligned).
+ * The symmetric form of Eq. 1 is the case z = 0 (pass a zero-filled array).
+ */
+int tf_pack_w8(const uint8_t* qweight, const uint8_t* zeros, const uint16_t* scales,
+               int64_t K, int64_t N, int group, void* packed, void* stream);
+
+/*
+ * Workspace needed by the GEMM entry points for this problem, in bytes
+ * (0 when none is needed).  Negative tf_status on bad arguments.
+ */
+int64_t tf_gemm_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group);
+
+/*
+ * Prefill GEMM (Section 2.1: M grows with the prompt length):
+ *   C_f16[M, N] = A_f16[M, K] x dequant(packed)[K, N], fp32 accumulate, RNE.
+ * Any M >= 1.  workspace may be NULL when tf_gemm_workspace_bytes is 0.
+ * The dequantized fp16 weight fed to the matrix cores is RNE(s * (q - z)),
+ * rounded once.
+ */
+int tf_w4a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,
+                  int64_t M, int64_t K, int64_t N, int group,
+                  void* workspace, size_t workspace_bytes, void* stream);
+int tf_w8a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,
+                  int64_t M, int64_t K, int64_t N, int group,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Decode GEMV (Section 2.1: batch-1 generation turns linear layers into
+ * matrix-vector products), 1 <= M <= TF_GEMV_MAX_M rows of A.
+ * Same operands and result as the GEMM; vector ALU only, fp32 accumulate.
+ */
+int tf_w4a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,
+                  int64_t M, int64_t K, int64_t N, int group, void* stream);
+int tf_w8a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,
+                  int64_t M, int64_t K, int64_t N, int group, void* stream);
+
+/*
+ * Debug / test exports.  They read the packed buffer through the same device
+ * unpack and dequantize code as the matmul kernels.
+ *   tf_unpack : q_out uint8 [K, N] and z_out uint8 [K/G, N] (Section 4.3 unpack)
+ *   tf_dequant: W_out [K, N] of s * (q - z) (Eq. 2), dtype TF_F16 (rounded
+ *               once, nearest even) or TF_F32 (exact).
+ */
+int tf_unpack(int bits, const void* packed, int64_t K, int64_t N, int group,
+              uint8_t* q_out, uint8_t* z_out, void* stream);
+int tf_dequant(int bits, const void* packed, int64_t K, int64_t N, int group,
+               int out_dtype, void* W_out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TILEFUSE_H */

@@ -1,0 +1,150 @@
+// C-ABI entry points of libtilefuse: argument validation (always before any
+// HIP call), layout sizing, and dispatch to the kernel launchers.
+#include "tf_internal.h"
+
+namespace {
+
+using tf::Layout;
+
+bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
+// Shape / format checks shared by every entry point.
+int check_weight(int bits, int64_t K, int64_t N, int group) {
+    if (bits != 4 && bits != 8) return TF_ERR_ARG;
+    if (group <= 0 || group % tf::kAtomK != 0) return TF_ERR_GROUP;
+    if (K <= 0 || N <= 0 || K > TF_MAX_DIM || N > TF_MAX_DIM) return TF_ERR_SHAPE;
+    if (K % group != 0 || N % 8 != 0) return TF_ERR_SHAPE;
+    return TF_OK;
+}
+
+int check_matmul(int bits, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
+                 int64_t K, int64_t N, int group) {
+    if (!A || !packed || !C) return TF_ERR_NULL;
+    int rc = check_weight(bits, K, N, group);
+    if (rc) return rc;
+    if (M < 1 || M > TF_MAX_M) return TF_ERR_SHAPE;
+    if (misaligned(A) || misaligned(packed) || misaligned(C)) return TF_ERR_ALIGN;
+    return TF_OK;
+}
+
+int gemm_entry(int bits, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
+               int64_t K, int64_t N, int group, void* ws, size_t ws_bytes, void* stream) {
+    int rc = check_matmul(bits, A, packed, C, M, K, N, group);
+    if (rc) return rc;
+    Layout L = tf::make_layout(bits, K, N, group);
+    int64_t need = tf::gemm_workspace_bytes(L, M);
+    if ((int64_t)ws_bytes < need) return TF_ERR_ARG;
+    if (need > 0 && !ws) return TF_ERR_NULL;
+    if (need > 0 && misaligned(ws)) return TF_ERR_ALIGN;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (M <= TF_GEMV_MAX_M) return tf::launch_gemv(L, A, packed, C, M, s);
+    return tf::launch_gemm(L, A, packed, C, M, ws, ws_bytes, s);
+}
+
+int gemv_entry(int bits, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
+               int64_t K, int64_t N, int group, void* stream) {
+    int rc = check_matmul(bits, A, packed, C, M, K, N, group);
+    if (rc) return rc;
+    if (M > TF_GEMV_MAX_M) return TF_ERR_ARG;
+    Layout L = tf::make_layout(bits, K, N, group);
+    return tf::launch_gemv(L, A, packed, C, M, static_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int tf_layout_version(void) { return tf::kLayoutVersion; }
+
+const char* tf_status_str(int status) {
+    switch (status) {
+        case TF_OK: return "ok";
+        case TF_ERR_NULL: return "null pointer argument";
+        case TF_ERR_SHAPE: return "bad shape (M, K, N, K % group, N % 8 or size limit)";
+        case TF_ERR_GROUP: return "group size must be a positive multiple of 32";
+        case TF_ERR_ALIGN: return "pointer not 16-byte aligned";
+        case TF_ERR_ARG: return "bad argument (bits, M for GEMV, dtype or workspace size)";
+        case TF_ERR_HIP: return "HIP runtime error at launch";
+        default: return "unknown status";
+    }
+}
+
+int64_t tf_packed_bytes(int bits, int64_t K, int64_t N, int group) {
+    int rc = check_weight(bits, K, N, group);
+    if (rc) return rc;
+    return tf::make_layout(bits, K, N, group).total;
+}
+
+int tf_pack_w4(const int32_t* qweight, const int32_t* qzeros, const uint16_t* scales, int64_t K,
+               int64_t N, int group, void* packed, void* stream) {
+    if (!qweight || !qzeros || !scales || !packed) return TF_ERR_NULL;
+    int rc = check_weight(4, K, N, group);
+    if (rc) return rc;
+    if (misaligned(qweight) || misaligned(qzeros) || misaligned(scales) || misaligned(packed))
+        return TF_ERR_ALIGN;
+    return tf::launch_pack_w4(qweight, qzeros, scales, tf::make_layout(4, K, N, group), packed,
+                              static_cast<hipStream_t>(stream));
+}
+
+int tf_pack_w8(const uint8_t* qweight, const uint8_t* zeros, const uint16_t* scales, int64_t K,
+               int64_t N, int group, void* packed, void* stream) {
+    if (!qweight || !zeros || !scales || !packed) return TF_ERR_NULL;
+    int rc = check_weight(8, K, N, group);
+    if (rc) return rc;
+    if (misaligned(qweight) || misaligned(zeros) || misaligned(scales) || misaligned(packed))
+        return TF_ERR_ALIGN;
+    return tf::launch_pack_w8(qweight, zeros, scales, tf::make_layout(8, K, N, group), packed,
+                              static_cast<hipStream_t>(stream));
+}
+
+int64_t tf_gemm_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group) {
+    int rc = check_weight(bits, K, N, group);
+    if (rc) return rc;
+    if (M < 1 || M > TF_MAX_M) return TF_ERR_SHAPE;
+    return tf::gemm_workspace_bytes(tf::make_layout(bits, K, N, group), M);
+}
+
+int tf_w4a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
+                  int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
+                  void* stream) {
+    return gemm_entry(4, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream);
+}
+
+int tf_w8a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
+                  int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
+                  void* stream) {
+    return gemm_entry(8, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream);
+}
+
+int tf_w4a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
+                  int64_t K, int64_t N, int group, void* stream) {
+    return gemv_entry(4, A_f16, packed, C_f16, M, K, N, group, stream);
+}
+
+int tf_w8a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
+                  int64_t K, int64_t N, int group, void* stream) {
+    return gemv_entry(8, A_f16, packed, C_f16, M, K, N, group, stream);
+}
+
+int tf_unpack(int bits, const void* packed, int64_t K, int64_t N, int group, uint8_t* q_out,
+              uint8_t* z_out, void* stream) {
+    if (!packed || !q_out || !z_out) return TF_ERR_NULL;
+    int rc = check_weight(bits, K, N, group);
+    if (rc) return rc;
+    if (misaligned(packed)) return TF_ERR_ALIGN;
+    return tf::launch_unpack(tf::make_layout(bits, K, N, group), packed, q_out, z_out,
+                             static_cast<hipStream_t>(stream));
+}
+
+int tf_dequant(int bits, const void* packed, int64_t K, int64_t N, int group, int out_dtype,
+               void* W_out, void* stream) {
+    if (!packed || !W_out) return TF_ERR_NULL;
+    int rc = check_weight(bits, K, N, group);
+    if (rc) return rc;
+    if (out_dtype != TF_F16 && out_dtype != TF_F32) return TF_ERR_ARG;
+    if (misaligned(packed) || misaligned(W_out)) return TF_ERR_ALIGN;
+    return tf::launch_dequant(tf::make_layout(bits, K, N, group), packed, out_dtype, W_out,
+                              static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,209 @@
+"""Python binding of libtilefuse (ctypes; argument marshalling only).
+
+Every computation runs in the library's HIP kernels; torch supplies device
+memory and the current stream.  The names mirror the C ABI in
+``include/tilefuse.h``.  There is no fallback: if the shared library is not
+built, importing the binding fails with an error that says how to build it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libtilefuse.so")
+
+TF_OK = 0
+TF_ERR_NULL = -1
+TF_ERR_SHAPE = -2
+TF_ERR_GROUP = -3
+TF_ERR_ALIGN = -4
+TF_ERR_ARG = -5
+TF_ERR_HIP = -6
+TF_F16 = 1
+TF_F32 = 2
+GEMV_MAX_M = 8
+
+EXPORTS = (
+    "tf_layout_version", "tf_status_str", "tf_packed_bytes", "tf_pack_w4", "tf_pack_w8",
+    "tf_gemm_workspace_bytes", "tf_w4a16_gemm", "tf_w8a16_gemm", "tf_w4a16_gemv",
+    "tf_w8a16_gemv", "tf_unpack", "tf_dequant",
+)
+
+
+class TileFuseError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_str(status)} (status {status})")
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libtilefuse.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing; build it with "
+                          "`python -m paper_2606_11357_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, I, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+    sig = {
+        "tf_layout_version": (I, []),
+        "tf_status_str": (ctypes.c_char_p, [I]),
+        "tf_packed_bytes": (I64, [I, I64, I64, I]),
+        "tf_pack_w4": (I, [P, P, P, I64, I64, I, P, P]),
+        "tf_pack_w8": (I, [P, P, P, I64, I64, I, P, P]),
+        "tf_gemm_workspace_bytes": (I64, [I, I64, I64, I64, I]),
+        "tf_w4a16_gemm": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
+        "tf_w8a16_gemm": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
+        "tf_w4a16_gemv": (I, [P, P, P, I64, I64, I64, I, P]),
+        "tf_w8a16_gemv": (I, [P, P, P, I64, I64, I64, I, P]),
+        "tf_unpack": (I, [I, P, I64, I64, I, P, P, P]),
+        "tf_dequant": (I, [I, P, I64, I64, I, I, P, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def status_str(status: int) -> str:
+    return load().tf_status_str(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != TF_OK:
+        raise TileFuseError(status, where)
+
+
+# ---------------------------------------------------------------------------
+# torch-facing wrappers
+# ---------------------------------------------------------------------------
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(device):
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _need_cuda(*tensors):
+    for t in tensors:
+        if t is not None and not t.is_cuda:
+            raise ValueError("tensors must be on the GPU (the library has no CPU path)")
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+
+
+def packed_bytes(bits: int, K: int, N: int, group: int = 128) -> int:
+    n = load().tf_packed_bytes(bits, K, N, group)
+    if n < 0:
+        raise TileFuseError(int(n), "tf_packed_bytes")
+    return int(n)
+
+
+def gemm_workspace_bytes(bits: int, M: int, K: int, N: int, group: int = 128) -> int:
+    n = load().tf_gemm_workspace_bytes(bits, M, K, N, group)
+    if n < 0:
+        raise TileFuseError(int(n), "tf_gemm_workspace_bytes")
+    return int(n)
+
+
+def pack_w4(qweight, qzeros, scales, K: int, N: int, group: int = 128, out=None):
+    """Pre-tile an AWQ 4-bit weight (int32 [K, N/8], int32 [K/G, N/8], fp16 [K/G, N])."""
+    torch = _torch()
+    _need_cuda(qweight, qzeros, scales)
+    if out is None:
+        out = torch.empty(packed_bytes(4, K, N, group), dtype=torch.uint8, device=qweight.device)
+    _check(load().tf_pack_w4(_ptr(qweight), _ptr(qzeros), _ptr(scales), K, N, group, _ptr(out),
+                             _stream(qweight.device)), "tf_pack_w4")
+    return out
+
+
+def pack_w8(qweight, zeros, scales, K: int, N: int, group: int = 128, out=None):
+    """Pre-tile an 8-bit weight (uint8 [K, N], uint8 [K/G, N], fp16 [K/G, N])."""
+    torch = _torch()
+    _need_cuda(qweight, zeros, scales)
+    if out is None:
+        out = torch.empty(packed_bytes(8, K, N, group), dtype=torch.uint8, device=qweight.device)
+    _check(load().tf_pack_w8(_ptr(qweight), _ptr(zeros), _ptr(scales), K, N, group, _ptr(out),
+                             _stream(qweight.device)), "tf_pack_w8")
+    return out
+
+
+def _matmul(name, A, packed, K, N, group, out, workspace=None):
+    torch = _torch()
+    _need_cuda(A, packed, out, workspace)
+    M = A.shape[0]
+    if A.dtype != torch.float16 or A.dim() != 2 or A.shape[1] != K:
+        raise ValueError("A must be fp16 [M, K]")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float16, device=A.device)
+    fn = getattr(load(), name)
+    if name.endswith("gemm"):
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        rc = fn(_ptr(A), _ptr(packed), _ptr(out), M, K, N, group, _ptr(workspace), ws_bytes,
+                _stream(A.device))
+    else:
+        rc = fn(_ptr(A), _ptr(packed), _ptr(out), M, K, N, group, _stream(A.device))
+    _check(rc, name)
+    return out
+
+
+def _gemm(bits, A, packed, K, N, group, out, workspace):
+    torch = _torch()
+    if workspace is None:
+        need = gemm_workspace_bytes(bits, A.shape[0], K, N, group)
+        if need:
+            workspace = torch.empty(need, dtype=torch.uint8, device=A.device)
+    return _matmul(f"tf_w{bits}a16_gemm", A, packed, K, N, group, out, workspace)
+
+
+def w4a16_gemm(A, packed, K: int, N: int, group: int = 128, out=None, workspace=None):
+    return _gemm(4, A, packed, K, N, group, out, workspace)
+
+
+def w8a16_gemm(A, packed, K: int, N: int, group: int = 128, out=None, workspace=None):
+    return _gemm(8, A, packed, K, N, group, out, workspace)
+
+
+def w4a16_gemv(A, packed, K: int, N: int, group: int = 128, out=None):
+    return _matmul("tf_w4a16_gemv", A, packed, K, N, group, out)
+
+
+def w8a16_gemv(A, packed, K: int, N: int, group: int = 128, out=None):
+    return _matmul("tf_w8a16_gemv", A, packed, K, N, group, out)
+
+
+def unpack(bits: int, packed, K: int, N: int, group: int = 128):
+    """Codes q [K, N] and zero-points z [K/G, N] read back from a packed buffer."""
+    torch = _torch()
+    _need_cuda(packed)
+    q = torch.empty((K, N), dtype=torch.uint8, device=packed.device)
+    z = torch.empty((K // group, N), dtype=torch.uint8, device=packed.device)
+    _check(load().tf_unpack(bits, _ptr(packed), K, N, group, _ptr(q), _ptr(z),
+                            _stream(packed.device)), "tf_unpack")
+    return q, z
+
+
+def dequant(bits: int, packed, K: int, N: int, group: int = 128, dtype=None):
+    """Dequantized weights [K, N] (fp16 rounded once, or exact fp32)."""
+    torch = _torch()
+    dtype = dtype or torch.float16
+    _need_cuda(packed)
+    code = {torch.float16: TF_F16, torch.float32: TF_F32}[dtype]
+    w = torch.empty((K, N), dtype=dtype, device=packed.device)
+    _check(load().tf_dequant(bits, _ptr(packed), K, N, group, code, _ptr(w),
+                             _stream(packed.device)), "tf_dequant")
+    return w

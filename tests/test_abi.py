@@ -1,0 +1,177 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, sizes the packed layout, and rejects bad arguments before it
+makes any HIP call (so these calls are safe without a device)."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2606_11357_amd import tilefuse as tfb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tilefuse.h")
+
+# fake device addresses: never dereferenced, because validation fails first
+P = ctypes.c_void_p(0x10000)          # 16-byte aligned
+P_ODD = ctypes.c_void_p(0x10008)      # 8-byte aligned only
+NULL = None
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tf_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return tfb.load()
+
+
+def test_header_declares_expected_entry_points():
+    assert header_functions() == sorted(tfb.EXPORTS)
+
+
+def test_library_exports_every_header_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", tfb.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (tf_[a-z0-9_]+)$", out, flags=re.M))
+    for name in header_functions():
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_version_and_status_strings(lib):
+    assert lib.tf_layout_version() == 1
+    for code in (tfb.TF_OK, tfb.TF_ERR_NULL, tfb.TF_ERR_SHAPE, tfb.TF_ERR_GROUP,
+                 tfb.TF_ERR_ALIGN, tfb.TF_ERR_ARG, tfb.TF_ERR_HIP):
+        s = tfb.status_str(code)
+        assert s and s != "unknown status"
+    assert tfb.status_str(12345) == "unknown status"
+
+
+def _layout_bytes(bits, K, N, G):
+    """Independent sizing of the packed layout: weights + fp16 scales + u8 zeros,
+    per panel of 64 (4-bit) or 32 (8-bit) columns, regions 256-byte aligned."""
+    pw = 64 if bits == 4 else 32
+    npan = -(-N // pw)
+    a256 = lambda v: -(-v // 256) * 256
+    return a256(npan * K * pw * bits // 8) + a256(npan * (K // G) * pw * 2) + a256(npan * (K // G) * pw)
+
+
+@pytest.mark.parametrize("bits,K,N,G", [(4, 4096, 14336, 128), (8, 4096, 4096, 128),
+                                        (4, 2048, 2048, 128), (4, 32768, 8192, 128),
+                                        (4, 256, 136, 64), (8, 96, 40, 32)])
+def test_packed_bytes(lib, bits, K, N, G):
+    assert lib.tf_packed_bytes(bits, K, N, G) == _layout_bytes(bits, K, N, G)
+
+
+def test_packed_bytes_headline_numbers(lib):
+    # K=4096, N=14336: 29,360,128 B of codes (same as the AWQ qweight), fp16
+    # scales 917,504 B (same), zero-points one byte each: 458,752 B
+    assert lib.tf_packed_bytes(4, 4096, 14336, 128) == 29360128 + 917504 + 458752
+
+
+@pytest.mark.parametrize("args,want", [
+    ((3, 256, 64, 128), tfb.TF_ERR_ARG),
+    ((4, 256, 64, 0), tfb.TF_ERR_GROUP),
+    ((4, 256, 64, 48), tfb.TF_ERR_GROUP),
+    ((4, 256, 64, -128), tfb.TF_ERR_GROUP),
+    ((4, 0, 64, 128), tfb.TF_ERR_SHAPE),
+    ((4, 256, 0, 128), tfb.TF_ERR_SHAPE),
+    ((4, 384, 64, 256), tfb.TF_ERR_SHAPE),      # K % G != 0
+    ((4, 256, 60, 128), tfb.TF_ERR_SHAPE),      # N % 8 != 0
+    ((8, 256, 12, 128), tfb.TF_ERR_SHAPE),
+    ((4, 65536 + 128, 64, 128), tfb.TF_ERR_SHAPE),
+])
+def test_packed_bytes_rejects(lib, args, want):
+    assert lib.tf_packed_bytes(*args) == want
+
+
+MATMUL_OK = dict(A=P, packed=P, C=P, M=4, K=256, N=64, G=128)
+
+
+def _gemv(lib, bits, **kw):
+    a = {**MATMUL_OK, **kw}
+    fn = lib.tf_w4a16_gemv if bits == 4 else lib.tf_w8a16_gemv
+    return fn(a["A"], a["packed"], a["C"], a["M"], a["K"], a["N"], a["G"], NULL)
+
+
+def _gemm(lib, bits, ws=NULL, ws_bytes=0, **kw):
+    a = {**MATMUL_OK, **kw}
+    fn = lib.tf_w4a16_gemm if bits == 4 else lib.tf_w8a16_gemm
+    return fn(a["A"], a["packed"], a["C"], a["M"], a["K"], a["N"], a["G"], ws, ws_bytes, NULL)
+
+
+BAD_MATMUL = [
+    (dict(A=NULL), tfb.TF_ERR_NULL),
+    (dict(packed=NULL), tfb.TF_ERR_NULL),
+    (dict(C=NULL), tfb.TF_ERR_NULL),
+    (dict(M=0), tfb.TF_ERR_SHAPE),
+    (dict(M=-1), tfb.TF_ERR_SHAPE),
+    (dict(K=0), tfb.TF_ERR_SHAPE),
+    (dict(N=-64), tfb.TF_ERR_SHAPE),
+    (dict(K=320), tfb.TF_ERR_SHAPE),           # K % 128 != 0
+    (dict(N=68), tfb.TF_ERR_SHAPE),            # N % 8 != 0
+    (dict(G=100), tfb.TF_ERR_GROUP),
+    (dict(A=P_ODD), tfb.TF_ERR_ALIGN),
+    (dict(packed=P_ODD), tfb.TF_ERR_ALIGN),
+    (dict(C=P_ODD), tfb.TF_ERR_ALIGN),
+]
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+@pytest.mark.parametrize("kw,want", BAD_MATMUL, ids=[str(b[0]) for b in BAD_MATMUL])
+def test_matmul_rejects(lib, bits, kw, want):
+    assert _gemv(lib, bits, **kw) == want
+    assert _gemm(lib, bits, **kw) == want
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_gemv_rejects_large_m(lib, bits):
+    assert _gemv(lib, bits, M=9) == tfb.TF_ERR_ARG
+    assert _gemv(lib, bits, M=4096) == tfb.TF_ERR_ARG
+
+
+def test_gemm_workspace_query(lib):
+    for bits, M, K, N in [(4, 2048, 4096, 14336), (8, 512, 4096, 4096), (4, 16, 2048, 2048)]:
+        n = lib.tf_gemm_workspace_bytes(bits, M, K, N, 128)
+        assert n >= 0
+    assert lib.tf_gemm_workspace_bytes(4, 0, 256, 64, 128) == tfb.TF_ERR_SHAPE
+    assert lib.tf_gemm_workspace_bytes(4, 16, 256, 64, 100) == tfb.TF_ERR_GROUP
+
+
+def test_pack_rejects(lib):
+    ok = (P, P, P, 256, 64, 128, P, NULL)
+    for fn in (lib.tf_pack_w4, lib.tf_pack_w8):
+        for i in (0, 1, 2, 6):
+            a = list(ok)
+            a[i] = NULL
+            assert fn(*a) == tfb.TF_ERR_NULL
+            a[i] = P_ODD
+            assert fn(*a) == tfb.TF_ERR_ALIGN
+        assert fn(P, P, P, 256, 60, 128, P, NULL) == tfb.TF_ERR_SHAPE
+        assert fn(P, P, P, 200, 64, 128, P, NULL) == tfb.TF_ERR_SHAPE
+        assert fn(P, P, P, 256, 64, 16, P, NULL) == tfb.TF_ERR_GROUP
+
+
+def test_unpack_dequant_reject(lib):
+    assert lib.tf_unpack(4, NULL, 256, 64, 128, P, P, NULL) == tfb.TF_ERR_NULL
+    assert lib.tf_unpack(4, P, 256, 64, 128, NULL, P, NULL) == tfb.TF_ERR_NULL
+    assert lib.tf_unpack(5, P, 256, 64, 128, P, P, NULL) == tfb.TF_ERR_ARG
+    assert lib.tf_unpack(4, P_ODD, 256, 64, 128, P, P, NULL) == tfb.TF_ERR_ALIGN
+    assert lib.tf_dequant(4, P, 256, 64, 128, 7, P, NULL) == tfb.TF_ERR_ARG
+    assert lib.tf_dequant(8, P, 256, 64, 128, tfb.TF_F16, NULL, NULL) == tfb.TF_ERR_NULL
+    assert lib.tf_dequant(8, P, 256, 64, 128, tfb.TF_F32, P_ODD, NULL) == tfb.TF_ERR_ALIGN
+    assert lib.tf_dequant(4, P, 250, 64, 128, tfb.TF_F32, P, NULL) == tfb.TF_ERR_SHAPE
+
+
+def test_binding_refuses_cpu_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(4, 256, dtype=torch.float16)
+    with pytest.raises(ValueError):
+        tfb.w4a16_gemv(x, torch.zeros(16, dtype=torch.uint8), 256, 64)

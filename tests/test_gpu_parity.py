@@ -1,0 +1,259 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bars:
+  * unpack (codes, zero-points): bit-exact;
+  * dequant: bit-exact, fp32 (exact Eq. 2) and fp16 (rounded once, RNE);
+  * matmul: max|gpu - oracle| <= 1e-2 * max|oracle| per output matrix (the
+    stated tolerance), and a stricter 1e-3 * max|oracle| regression bound that
+    a dropped K term would already break;
+  * integer invariant (s = 1, z = 0, integer activations): bit-exact against
+    RNE_fp16 of the exact integer matmul;
+  * bitwise reproducibility, and canaries around every output.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_11357_amd.synth import make_inputs, pack_nibbles
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2          # stated tolerance, relative to max|oracle| per output matrix
+STRICT = 1e-3       # internal regression bound
+GUARD = 4096        # canary elements on each side of an output
+
+
+@pytest.fixture(scope="module")
+def tf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_11357_amd import tilefuse
+    tilefuse.load()
+    return tilefuse
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def pack(tf, d):
+    K, N, G = d["K"], d["N"], d["group"]
+    if d["bits"] == 4:
+        return tf.pack_w4(dev(d["qweight"]), dev(d["qzeros"]), dev(d["s"]), K, N, G)
+    return tf.pack_w8(dev(d["qweight"]), dev(d["zeros"]), dev(d["s"]), K, N, G)
+
+
+def guarded_out(M, N):
+    buf = torch.full((M * N + 2 * GUARD,), -7.0, dtype=torch.float16, device="cuda")
+    return buf, buf[GUARD:GUARD + M * N].view(M, N)
+
+
+def check_guard(buf):
+    g = torch.cat([buf[:GUARD], buf[-GUARD:]]).float().cpu().numpy()
+    assert np.all(g == -7.0), "write outside the output"
+
+
+def run(tf, kind, d, packed, x=None):
+    K, N, G = d["K"], d["N"], d["group"]
+    x = d["x"] if x is None else x
+    M = x.shape[0]
+    buf, out = guarded_out(M, N)
+    fn = getattr(tf, f"w{d['bits']}a16_{kind}")
+    fn(dev(x), packed, K, N, G, out=out)
+    torch.cuda.synchronize()
+    check_guard(buf)
+    return out.cpu().numpy()
+
+
+def ref(d, x=None, cols=None):
+    x = d["x"] if x is None else x
+    q, z, s = d["q"], d["z"], d["s"]
+    if cols is not None:
+        q, z, s = q[:, cols], z[:, cols], s[:, cols]
+    return oracle.matmul(x, oracle.dequant(q, z, s, d["group"]))
+
+
+def assert_parity(gpu, want, what=""):
+    gpu = gpu.astype(np.float64)
+    assert np.all(np.isfinite(gpu)), what
+    scale = np.abs(want).max()
+    err = np.abs(gpu - want).max()
+    assert err <= TOL * scale, f"{what}: max err {err:.4g} > {TOL} * {scale:.4g}"
+    assert err <= STRICT * scale, f"{what}: max err {err:.4g} > {STRICT} * {scale:.4g}"
+    return err / scale
+
+
+# ---------------------------------------------------------------------------
+# unpack / dequant: bit-exact
+# ---------------------------------------------------------------------------
+SMALL = [(4, 256, 136, 128), (4, 128, 64, 32), (4, 2048, 2048, 128), (8, 256, 40, 128),
+         (8, 192, 96, 64), (8, 4096, 4096, 128), (4, 96, 8, 32)]
+
+
+@pytest.mark.parametrize("bits,K,N,G", SMALL)
+def test_unpack_bitexact(tf, bits, K, N, G):
+    d = make_inputs(bits, 1, K, N, group=G, seed=K + N)
+    q, z = tf.unpack(bits, pack(tf, d), K, N, G)
+    np.testing.assert_array_equal(q.cpu().numpy(), d["q"])
+    np.testing.assert_array_equal(z.cpu().numpy(), d["z"])
+    if bits == 4:   # the oracle's own unpack of the boundary words agrees
+        np.testing.assert_array_equal(oracle.unpack_w4(d["qweight"]), d["q"])
+
+
+@pytest.mark.parametrize("bits,K,N,G", SMALL)
+def test_dequant_bitexact(tf, bits, K, N, G):
+    d = make_inputs(bits, 1, K, N, group=G, seed=K * 3 + N)
+    packed = pack(tf, d)
+    w64 = oracle.dequant(d["q"], d["z"], d["s"], G)
+    w32 = tf.dequant(bits, packed, K, N, G, dtype=torch.float32).cpu().numpy()
+    np.testing.assert_array_equal(w32.view(np.uint32), w64.astype(np.float32).view(np.uint32))
+    w16 = tf.dequant(bits, packed, K, N, G, dtype=torch.float16).cpu().numpy()
+    np.testing.assert_array_equal(w16.view(np.uint16), oracle.dequant_f16(d["q"], d["z"], d["s"], G).view(np.uint16))
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_dequant_extreme_scales(tf, bits):
+    """Scales from subnormal to the largest finite fp16, every code/zero pair."""
+    qmax = (1 << bits) - 1
+    K, G = 256 if bits == 8 else 32, 32
+    N = 64
+    rng = np.random.default_rng(99)
+    q = np.tile(np.arange(K, dtype=np.int64)[:, None] % (qmax + 1), (1, N)).astype(np.uint8)
+    z = rng.integers(0, qmax + 1, size=(K // G, N), dtype=np.uint8)
+    sb = np.array([0x0001, 0x0002, 0x03FF, 0x0400, 0x1000, 0x2118, 0x3C00, 0x5000, 0x7BFF,
+                   0x8001, 0xBC00, 0x0155, 0x1A2B, 0x2E66, 0x7800, 0x0010], dtype=np.uint16)
+    s = np.tile(sb, (K // G, N // sb.size)).view(np.float16)
+    d = {"bits": bits, "K": K, "N": N, "group": G, "q": q, "z": z, "s": s}
+    if bits == 4:
+        d["qweight"], d["qzeros"] = pack_nibbles(q), pack_nibbles(z)
+    else:
+        d["qweight"], d["zeros"] = q, z
+    packed = pack(tf, d)
+    with np.errstate(over="ignore"):
+        want16 = oracle.dequant_f16(q, z, s, G)
+    w16 = tf.dequant(bits, packed, K, N, G, dtype=torch.float16).cpu().numpy()
+    np.testing.assert_array_equal(w16.view(np.uint16), want16.view(np.uint16))
+    w32 = tf.dequant(bits, packed, K, N, G, dtype=torch.float32).cpu().numpy()
+    np.testing.assert_array_equal(w32, oracle.dequant(q, z, s, G).astype(np.float32))
+
+
+# ---------------------------------------------------------------------------
+# matmul parity on small and ragged shapes (full comparison)
+# ---------------------------------------------------------------------------
+RAGGED = [(4, 1, 256, 136, 128), (4, 3, 128, 72, 32), (4, 8, 512, 200, 128),
+          (8, 5, 256, 40, 128), (8, 8, 192, 104, 64), (4, 7, 96, 8, 32),
+          (8, 2, 4096, 4096, 128), (4, 4, 2048, 2048, 128)]
+
+
+@pytest.mark.parametrize("bits,M,K,N,G", RAGGED)
+def test_gemv_parity_small(tf, bits, M, K, N, G):
+    d = make_inputs(bits, M, K, N, group=G, seed=M + K + N)
+    assert_parity(run(tf, "gemv", d, pack(tf, d)), ref(d), f"gemv {bits} {M}x{K}x{N}")
+
+
+GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 200, 64),
+               (8, 33, 256, 40, 128), (8, 130, 384, 104, 128), (4, 9, 96, 8, 32),
+               (4, 300, 1024, 520, 128), (8, 64, 128, 4096, 128), (4, 1, 256, 64, 128)]
+
+
+@pytest.mark.parametrize("bits,M,K,N,G", GEMM_SHAPES)
+def test_gemm_parity_small(tf, bits, M, K, N, G):
+    d = make_inputs(bits, M, K, N, group=G, seed=M * 7 + K + N)
+    assert_parity(run(tf, "gemm", d, pack(tf, d)), ref(d), f"gemm {bits} {M}x{K}x{N}")
+
+
+@pytest.mark.parametrize("kind,bits,M,K,N", [("gemv", 4, 8, 4096, 1024), ("gemv", 8, 8, 4096, 512),
+                                             ("gemm", 8, 256, 4096, 512), ("gemm", 4, 200, 8192, 256),
+                                             ("gemv", 4, 1, 32768, 64)])
+def test_integer_invariant_bitexact(tf, kind, bits, M, K, N):
+    """s = 1, z = 0, integer x in [-3, 3]: every partial sum is an integer below
+    2^24, so the fp16 output must be RNE of the exact integer matmul."""
+    rng = np.random.default_rng(1234 + M)
+    G = 128
+    xi = rng.integers(-3, 4, size=(M, K))
+    qi = rng.integers(0, 1 << bits, size=(K, N), dtype=np.uint8)
+    if bits == 8:
+        qi = (qi // 8).astype(np.uint8)      # keep |y| below the fp16 range limit
+    z = np.zeros((K // G, N), dtype=np.uint8)
+    d = {"bits": bits, "K": K, "N": N, "group": G, "q": qi, "z": z,
+         "s": np.ones((K // G, N), dtype=np.float16), "x": xi.astype(np.float16)}
+    if bits == 4:
+        d["qweight"], d["qzeros"] = pack_nibbles(qi), pack_nibbles(z)
+    else:
+        d["qweight"], d["zeros"] = qi, z
+    exact = xi.astype(np.int64) @ qi.astype(np.int64)
+    assert np.abs(exact).max() < 65504
+    got = run(tf, kind, d, pack(tf, d))
+    np.testing.assert_array_equal(got.view(np.uint16), exact.astype(np.float64).astype(np.float16).view(np.uint16))
+
+
+def test_closed_form(tf):
+    """x = 1, q = 9, z = 2, s = 1/64 per column: y = K * 7 / 64 exactly."""
+    K, N, G = 1024, 128, 128
+    for bits in (4, 8):
+        q = np.full((K, N), 9, dtype=np.uint8)
+        z = np.full((K // G, N), 2, dtype=np.uint8)
+        d = {"bits": bits, "K": K, "N": N, "group": G, "q": q, "z": z,
+             "s": np.full((K // G, N), 1 / 64, dtype=np.float16)}
+        if bits == 4:
+            d["qweight"], d["qzeros"] = pack_nibbles(q), pack_nibbles(z)
+        else:
+            d["qweight"], d["zeros"] = q, z
+        packed = pack(tf, d)
+        for kind, M in (("gemv", 3), ("gemm", 40)):
+            got = run(tf, kind, d, packed, x=np.ones((M, K), dtype=np.float16))
+            np.testing.assert_array_equal(got, np.full((M, N), K * 7 / 64, dtype=np.float16))
+
+
+@pytest.mark.parametrize("kind,M", [("gemv", 1), ("gemv", 8), ("gemm", 300)])
+def test_bitwise_reproducible(tf, kind, M):
+    d = make_inputs(4, M, 2048, 1024, seed=5)
+    packed = pack(tf, d)
+    a = run(tf, kind, d, packed)
+    b = run(tf, kind, d, packed)
+    np.testing.assert_array_equal(a.view(np.uint16), b.view(np.uint16))
+
+
+# ---------------------------------------------------------------------------
+# the Llama-shaped workloads at full size
+# ---------------------------------------------------------------------------
+def _sample_cols(N, rng, n=256):
+    return np.sort(rng.choice(N, size=min(n, N), replace=False))
+
+
+@pytest.mark.parametrize("M", [1, 4, 8])
+def test_gemv_w4_k4096_n14336_full(tf, M):
+    d = make_inputs(4, M, 4096, 14336, seed=0)
+    assert_parity(run(tf, "gemv", d, pack(tf, d)), ref(d), f"W4 GEMV M={M}")
+
+
+def test_w8_k4096_n4096_full(tf):
+    d = make_inputs(8, 1, 4096, 4096, seed=0)
+    assert_parity(run(tf, "gemv", d, pack(tf, d)), ref(d), "W8 GEMV M=1")
+    d = make_inputs(8, 512, 4096, 4096, seed=0)
+    assert_parity(run(tf, "gemm", d, pack(tf, d)), ref(d), "W8 GEMM M=512")
+
+
+def test_gemm_w4_m16_k2048_n2048_full(tf):
+    d = make_inputs(4, 16, 2048, 2048, seed=0)
+    assert_parity(run(tf, "gemm", d, pack(tf, d)), ref(d), "W4 GEMM M=16")
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("M,K,N,xstd", [(2048, 4096, 14336, 1.0), (2048, 14336, 4096, 1.0),
+                                         (1024, 4096, 32768, 0.5), (1024, 32768, 8192, 0.5)])
+def test_gemm_w4_large_sampled(tf, M, K, N, xstd):
+    """Full-size launch; outputs compared on sampled rows x sampled columns, and
+    all of C checked finite."""
+    d = make_inputs(4, M, K, N, seed=0, x_std=xstd)
+    got = run(tf, "gemm", d, pack(tf, d))
+    assert np.all(np.isfinite(got.astype(np.float64)))
+    rng = np.random.default_rng(M + K + N)
+    rows = np.sort(np.concatenate([[0, M - 1], rng.choice(M, size=30, replace=False)]))
+    cols = np.sort(np.concatenate([[0, N - 1], _sample_cols(N, rng, 510)]))
+    cols = np.unique(cols)
+    want = ref(d, x=d["x"][rows], cols=cols)
+    assert_parity(got[np.ix_(rows, cols)], want, f"W4 GEMM {M}x{K}x{N} sampled")
