@@ -45,14 +45,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-cols", type=int, default=1024)
     return ap.parse_args()
 
 
-def cpu_baseline(sample_cols):
-    """The oracle (fp64, numpy/BLAS) timed on the host on a bounded sample of
-    the prefill workload: all M=2048 rows, K=4096, the first `sample_cols`
-    output columns of the N=14336 weight."""
+def cpu_baseline():
+    """The oracle (fp64, numpy/BLAS) timed on the host on the same prefill
+    GEMM pair (both shapes, full size) and on one decode GEMV."""
     import oracle
     from paper_2606_11357_amd.synth import make_inputs
     try:
@@ -60,17 +58,26 @@ def cpu_baseline(sample_cols):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count()
-    M, K, N = GEMM_SHAPES[0]
-    d = make_inputs(4, M, K, sample_cols, seed=0)
+    t_gemm, flops = 0.0, 0.0
+    for (M, K, N) in GEMM_SHAPES:
+        d = make_inputs(4, M, K, N, group=GROUP, seed=0)
+        t0 = time.perf_counter()
+        y = oracle.w4a16(d["x"], d["qweight"], d["qzeros"], d["s"], GROUP)
+        t_gemm += time.perf_counter() - t0
+        flops += 2.0 * M * N * K
+        assert np.isfinite(y).all()
+        del d, y
+    M1, K1, N1 = GEMV_SHAPE
+    d = make_inputs(4, M1, K1, N1, group=GROUP, seed=0)
     t0 = time.perf_counter()
-    y = oracle.w4a16(d["x"], d["qweight"], d["qzeros"], d["s"], GROUP)
-    t = time.perf_counter() - t0
-    assert np.isfinite(y).all()
-    flops = 2.0 * M * K * sample_cols
-    return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": int(threads),
-            "kind": "oracle", "seconds": round(t, 3),
-            "sample": f"W4A16 oracle (unpack, fp64 dequant, fp64 matmul) at M={M}, K={K}, "
-                      f"first {sample_cols} of N={N} columns"}
+    oracle.w4a16(d["x"], d["qweight"], d["qzeros"], d["s"], GROUP)
+    t_gemv = time.perf_counter() - t0
+    return {"value": round(flops / t_gemm / 1e12, 4), "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle", "seconds": round(t_gemm, 3),
+            "gemv_GBps": round(algo_bytes_w4(K1, N1) / t_gemv / 1e9, 3),
+            "gemv_seconds": round(t_gemv, 4),
+            "sample": "the whole prefill GEMM pair of one step (M=2048; K,N = 4096,14336 and "
+                      "14336,4096) plus one M=1 GEMV, oracle = unpack + fp64 dequant + fp64 BLAS matmul"}
 
 
 def main():
@@ -146,7 +153,6 @@ def main():
     gemv_us = gemv_ms * 1e3 / GEMV_REPS
     gemv_bytes = algo_bytes_w4(K1, N1)
     gemv_gbs = gemv_bytes / (gemv_us * 1e-6) / 1e9
-    gemm_us_each = [None, None]
 
     line = {
         "metric": "W4A16 GEMM TFLOP/s (M=2048) + GEMV eff. HBM GB/s (M=1), % of roofline",
@@ -188,9 +194,8 @@ def main():
         },
         "gemm_ms": round(gemm_ms, 4),
     }
-    del gemm_us_each
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(args.cpu_sample_cols)
+        line["cpu_baseline"] = cpu_baseline()
     print(json.dumps(line), flush=True)
 
 

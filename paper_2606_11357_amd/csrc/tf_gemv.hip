@@ -4,119 +4,263 @@
 // y[m, n] = sum_k x[m, k] * s[g, n] * (q[k, n] - z[g, n]),  1 <= M <= 8.
 //
 // Mapping (the GPU form of the principle of Section 4.4: every compute unit
-// streams its own weight slice, activations are shared, each workgroup owns
-// distinct outputs and no partial sums leave it):
-//  - one workgroup per panel of PW columns, all of K;
-//  - each wave streams whole 1 KiB atoms (one 16-byte load per lane);
-//  - a lane owns T columns x 8 rows of an atom, so one 16-byte slice of x per
-//    activation row is reused across its T columns (the widening idea of
-//    Section 4.3: one activation fragment feeds many outputs);
-//  - per group the lane accumulates sum_k x * (q - z) with v_dot2_f32_f16 on
-//    exact fp16 integer pairs, then applies s once per group (Eq. 2 factored
-//    over the group: s is constant on it);
-//  - the four lanes sharing a column combine with cross-lane shuffles, the
-//    waves through LDS, in a fixed order (bitwise reproducible).
+// streams its own weight slice, the activations are shared, each workgroup
+// owns distinct outputs and no partial sum leaves it):
+//  - one workgroup per panel of PW output columns, all of K;
+//  - K is walked in segments of KSEG rows; per segment every wave issues the
+//    loads of all its U atoms at once (one 16-byte load per lane per atom)
+//    and the loads of the next segment before it computes the current one,
+//    so the whole weight stream is in flight early;
+//  - the segment's activations and metadata are staged once in LDS;
+//  - a lane owns T columns x 8 rows of an atom: one 16-byte activation slice
+//    per row of A feeds its T columns (the widening idea of Section 4.3: one
+//    activation fragment reused across many outputs).
+// Arithmetic (Eq. 2 summed over a group, where s and z are constant):
+//    sum_k x (s (q - z)) = s * (sum_k x q - z * sum_k x).
+//  - M < 4: codes are read as exact fp16 integers 1024 + q (or 1024 + 16 q,
+//    which needs no shift) and dotted with x by v_dot2_f32_f16; the offsets
+//    and z are removed per group with the per-lane sums of x.
+//  - M >= 4: each weight is dequantized once to fp16 with the GEMM's code,
+//    RNE(s (q - z)), and dotted with all M rows of x.
+// All sums are fp32.  Lanes sharing a column combine by cross-lane shuffles,
+// the waves through LDS, in a fixed order: results are bitwise reproducible.
 #include "tf_internal.h"
 
 namespace tf {
 namespace {
 
-constexpr int kGemvThreads = 256;
-constexpr int kGemvWaves = kGemvThreads / 64;
+template <int BITS, int M, int WAVES, int U>
+struct GemvCfg {
+    static constexpr int T = BITS == 4 ? 4 : 2;      // columns per lane
+    static constexpr int PW = BITS == 4 ? 64 : 32;   // panel width
+    static constexpr int ROUND_ATOMS = WAVES * U;    // atoms of one round of the workgroup
+    static constexpr int XB = U * kAtomK * 2;        // bytes of one row of x per wave-round
+    static constexpr int SB = U * PW * 2;            // scale bytes of up to U groups
+    static constexpr int ZB = U * PW;                // zero-point bytes of up to U groups
+    static constexpr bool FACT = M < 4;
+    static_assert(XB == 512 && SB <= 1024 && ZB <= 512, "one cooperative load per lane each");
+};
 
-template <int BITS, int M>
-__global__ __launch_bounds__(kGemvThreads) void gemv_kernel(
+// One wave's staging area in LDS (private to the wave: no barrier needed).
+template <int M, int U, int PW>
+struct WaveStage {
+    uint64_t x[M][U * kAtomK / 4];     // M rows x U*32 halves
+    u32x4 s[U * PW * 2 / 16];
+    uint64_t z[U * PW / 8];
+};
+
+template <int BITS, int M, int WAVES, int U>
+__global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
     int K, int N, int group, int64_t s_off, int64_t z_off, int na, int ng) {
-    constexpr int T = BITS == 4 ? 4 : 2;         // columns per lane
-    constexpr int PW = BITS == 4 ? 64 : 32;      // panel width
-    const int p = blockIdx.x;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int c = lane & 15, kg = lane >> 4;
+    using Cfg = GemvCfg<BITS, M, WAVES, U>;
+    constexpr int T = Cfg::T, PW = Cfg::PW, RA = Cfg::ROUND_ATOMS;
+    constexpr bool FACT = Cfg::FACT;
+    constexpr int NT = WAVES * 64;
+    using Stage = WaveStage<M, U, PW>;
+    union Smem {
+        Stage st[WAVES];
+        float red[WAVES][M][PW];
+    };
+    __shared__ __align__(16) Smem sm;
 
-    float acc[M][T];
+    const int p = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar) index math
+    const int c = lane & 15, kg = lane >> 4;
+    const int apg = group / kAtomK;
+    const u32x4* wpanel = reinterpret_cast<const u32x4*>(packed) + (int64_t)p * na * 64 + lane;
+    const uint8_t* spanel = packed + s_off + (int64_t)p * ng * PW * 2;
+    const uint8_t* zpanel = packed + z_off + (int64_t)p * ng * PW;
+    const int64_t s_last = ((int64_t)ng * PW * 2 - 16);     // last 16-byte slot of the panel's scales
+    const int64_t z_last = ((int64_t)ng * PW - 8);
+    const int rounds = (na + RA - 1) / RA;
+    Stage& st = sm.st[wave];
+
+    float y[M][T];
 #pragma unroll
     for (int m = 0; m < M; ++m)
 #pragma unroll
-        for (int t = 0; t < T; ++t) acc[m][t] = 0.f;
+        for (int t = 0; t < T; ++t) y[m][t] = 0.f;
 
-    const uint4* wbase = reinterpret_cast<const uint4*>(packed) + (int64_t)p * na * 64 + lane;
-    const uint16_t* sbase = reinterpret_cast<const uint16_t*>(packed + s_off) + (int64_t)p * ng * PW + c * T;
-    const uint8_t* zbase = packed + z_off + (int64_t)p * ng * PW + c * T;
-    const int atoms_per_group = group / kAtomK;
-
-    // Each wave takes whole groups; inside a group it walks the group's atoms.
-    for (int g = wave; g < ng; g += kGemvWaves) {
-        float part[M][T];
+    // Loads of one round: first the wave's slice of x and its groups'
+    // metadata (small), then its U weight atoms.  Addresses are clamped into
+    // the panel so every load is in bounds and the code stays branch-free;
+    // atoms past K are skipped at use.
+    struct Buf {
+        uint64_t xr[M];
+        u32x4 sr;
+        uint64_t zr;
+        u32x4 w[U];
+    };
+    auto issue = [&](int r, Buf& b) {
+        const int a0 = r * RA + wave * U;
+        const int k0 = min(a0, na - 1) * kAtomK;
 #pragma unroll
-        for (int m = 0; m < M; ++m)
-#pragma unroll
-            for (int t = 0; t < T; ++t) part[m][t] = 0.f;
-
-        uint32_t negz[T];
-        _Float16 sc[T];
-        {
-            const uint16_t* sp = sbase + (int64_t)g * PW;
-            const uint8_t* zp = zbase + (int64_t)g * PW;
-#pragma unroll
-            for (int t = 0; t < T; ++t) {
-                sc[t] = __builtin_bit_cast(_Float16, sp[t]);
-                negz[t] = neg_zero_pair(zp[t]);
-            }
+        for (int m = 0; m < M; ++m) {
+            const int k = min(k0 + 4 * lane, K - 4);
+            b.xr[m] = *reinterpret_cast<const uint64_t*>(A + (int64_t)m * K + k);
         }
-        for (int ai = 0; ai < atoms_per_group; ++ai) {
-            const int a = g * atoms_per_group + ai;
-            const uint4 wv = wbase[(int64_t)a * 64];
-            const int k0 = a * kAtomK + 8 * kg;
-            uint4 xv[M];
+        const int g0 = min(a0, na - 1) / apg;
+        b.sr = *reinterpret_cast<const u32x4*>(spanel + min((int64_t)g0 * PW * 2 + 16 * lane, s_last));
+        b.zr = *reinterpret_cast<const uint64_t*>(zpanel + min((int64_t)g0 * PW + 8 * lane, z_last));
+#pragma unroll
+        for (int i = 0; i < U; ++i)
+            b.w[i] = __builtin_nontemporal_load(wpanel + (int64_t)min(a0 + i, na - 1) * 64);
+    };
+
+    auto consume = [&](int r, Buf& b) {
+        const int a0 = r * RA + wave * U;
+        if (a0 >= na) return;
+        const int g0 = a0 / apg;
+        int pos = a0 - g0 * apg;      // atom a0's place inside its group
+        int gl = 0;                   // current group, relative to g0
+        // stage this wave's x slice and metadata (wave-private LDS)
+#pragma unroll
+        for (int m = 0; m < M; ++m) st.x[m][lane] = b.xr[m];
+        if (16 * lane < Cfg::SB) st.s[lane] = b.sr;
+        if (8 * lane < Cfg::ZB) st.z[lane] = b.zr;
+
+        float alo[M][T], ahi[M][T], sxlo[M], sxhi[M];
+        auto reset = [&]() {
+#pragma unroll
+            for (int m = 0; m < M; ++m) {
+                sxlo[m] = 0.f;
+                sxhi[m] = 0.f;
+#pragma unroll
+                for (int t = 0; t < T; ++t) {
+                    alo[m][t] = 0.f;
+                    ahi[m][t] = 0.f;
+                }
+            }
+        };
+        reset();
+        const half2_t ones = {(_Float16)1.0f, (_Float16)1.0f};
+        const uint8_t* sbytes = reinterpret_cast<const uint8_t*>(st.s);
+        const uint8_t* zbytes = reinterpret_cast<const uint8_t*>(st.z);
+
+#pragma unroll
+        for (int i = 0; i < U; ++i) {
+            const int a = a0 + i;
+            if (a >= na) break;
+            u32x4 xv[M];
 #pragma unroll
             for (int m = 0; m < M; ++m)
-                xv[m] = *reinterpret_cast<const uint4*>(A + (int64_t)m * K + k0);
-            const uint32_t wd[4] = {wv.x, wv.y, wv.z, wv.w};
-            if constexpr (BITS == 4) {
+                xv[m] = *reinterpret_cast<const u32x4*>(&st.x[m][(i * kAtomK + 8 * kg) / 4]);
+            const uint32_t wd[4] = {b.w[i][0], b.w[i][1], b.w[i][2], b.w[i][3]};
+            if constexpr (!FACT) {
+                // dequantize once per weight (the GEMM's code: RNE(s (q - z))) and
+                // let every row of A reuse it
+                const uint8_t* zp = zbytes + gl * PW + c * T;
+                const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
 #pragma unroll
                 for (int t = 0; t < T; ++t) {
-                    uint32_t cp[4];
-                    w4_code_pairs(wd[t], cp);
-                    half2_t d[4];
-#pragma unroll
-                    for (int pr = 0; pr < 4; ++pr) d[pr] = as_h2(cp[pr]) + as_h2(negz[t]);
+                    const uint32_t sb = sp[t];
+                    const half2_t s2 = as_h2(sb | (sb << 16));
+                    half8_t w8;
+                    if constexpr (BITS == 4)
+                        w8 = dq_w4_dword(wd[t], neg_zero_pair(zp[t]), s2);
+                    else
+                        w8 = dq_w8_dwords(wd[2 * t], wd[2 * t + 1], neg_zero_pair(zp[t]), s2);
+                    const half2_t w2[4] = {{w8[0], w8[1]}, {w8[2], w8[3]}, {w8[4], w8[5]}, {w8[6], w8[7]}};
 #pragma unroll
                     for (int m = 0; m < M; ++m) {
-                        const uint32_t xd[4] = {xv[m].x, xv[m].y, xv[m].z, xv[m].w};
-                        float v = part[m][t];
+                        float v = y[m][t];
 #pragma unroll
                         for (int pr = 0; pr < 4; ++pr)
-                            v = __builtin_amdgcn_fdot2(d[pr], as_h2(xd[pr]), v, false);
-                        part[m][t] = v;
+                            v = __builtin_amdgcn_fdot2(w2[pr], as_h2(xv[m][pr]), v, false);
+                        y[m][t] = v;
                     }
                 }
-            } else {
+                if (++pos == apg) {
+                    pos = 0;
+                    ++gl;
+                }
+                continue;
+            }
 #pragma unroll
-                for (int t = 0; t < T; ++t) {
-                    uint32_t cp[4];
-                    w8_code_pairs(wd[2 * t], cp);
-                    w8_code_pairs(wd[2 * t + 1], cp + 2);
-                    half2_t d[4];
+            for (int t = 0; t < T; ++t) {
+                uint32_t P[4];
+                if constexpr (BITS == 4) {
+                    w4_code_pairs_x16(wd[t], P);
+                } else {
+                    w8_code_pairs(wd[2 * t], P);
+                    w8_code_pairs(wd[2 * t + 1], P + 2);
+                }
 #pragma unroll
-                    for (int pr = 0; pr < 4; ++pr) d[pr] = as_h2(cp[pr]) + as_h2(negz[t]);
-#pragma unroll
-                    for (int m = 0; m < M; ++m) {
-                        const uint32_t xd[4] = {xv[m].x, xv[m].y, xv[m].z, xv[m].w};
-                        float v = part[m][t];
-#pragma unroll
-                        for (int pr = 0; pr < 4; ++pr)
-                            v = __builtin_amdgcn_fdot2(d[pr], as_h2(xd[pr]), v, false);
-                        part[m][t] = v;
+                for (int m = 0; m < M; ++m) {
+                    const uint32_t xd[4] = {xv[m][0], xv[m][1], xv[m][2], xv[m][3]};
+                    float lo = alo[m][t], hi = ahi[m][t];
+                    lo = __builtin_amdgcn_fdot2(as_h2(P[0]), as_h2(xd[0]), lo, false);
+                    lo = __builtin_amdgcn_fdot2(as_h2(P[2]), as_h2(xd[2]), lo, false);
+                    if constexpr (BITS == 4) {
+                        hi = __builtin_amdgcn_fdot2(as_h2(P[1]), as_h2(xd[1]), hi, false);
+                        hi = __builtin_amdgcn_fdot2(as_h2(P[3]), as_h2(xd[3]), hi, false);
+                    } else {
+                        lo = __builtin_amdgcn_fdot2(as_h2(P[1]), as_h2(xd[1]), lo, false);
+                        lo = __builtin_amdgcn_fdot2(as_h2(P[3]), as_h2(xd[3]), lo, false);
                     }
+                    alo[m][t] = lo;
+                    ahi[m][t] = hi;
                 }
             }
+            if constexpr (FACT) {
+#pragma unroll
+                for (int m = 0; m < M; ++m) {
+                    const uint32_t xd[4] = {xv[m][0], xv[m][1], xv[m][2], xv[m][3]};
+                    float lo = sxlo[m], hi = sxhi[m];
+                    lo = __builtin_amdgcn_fdot2(as_h2(xd[0]), ones, lo, false);
+                    lo = __builtin_amdgcn_fdot2(as_h2(xd[2]), ones, lo, false);
+                    if constexpr (BITS == 4) {
+                        hi = __builtin_amdgcn_fdot2(as_h2(xd[1]), ones, hi, false);
+                        hi = __builtin_amdgcn_fdot2(as_h2(xd[3]), ones, hi, false);
+                    } else {
+                        lo = __builtin_amdgcn_fdot2(as_h2(xd[1]), ones, lo, false);
+                        lo = __builtin_amdgcn_fdot2(as_h2(xd[3]), ones, lo, false);
+                    }
+                    sxlo[m] = lo;
+                    sxhi[m] = hi;
+                }
+            }
+            // close the group at its last atom or at the end of this wave's run
+            const bool group_end = ++pos == apg;
+            if (group_end || i == U - 1 || a + 1 == na) {
+                const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
+                const uint8_t* zp = zbytes + gl * PW + c * T;
+#pragma unroll
+                for (int t = 0; t < T; ++t) {
+                    const float s = (float)__builtin_bit_cast(_Float16, sp[t]);
+                    if constexpr (FACT) {
+                        const float zf = (float)zp[t];
+#pragma unroll
+                        for (int m = 0; m < M; ++m) {
+                            float v;
+                            if constexpr (BITS == 4) {
+                                v = fmaf(ahi[m][t], 0.0625f, alo[m][t]);
+                                v = fmaf(-(1024.f + zf), sxlo[m], v);
+                                v = fmaf(-(64.f + zf), sxhi[m], v);
+                            } else {
+                                v = fmaf(-(1024.f + zf), sxlo[m], alo[m][t]);
+                            }
+                            y[m][t] = fmaf(s, v, y[m][t]);
+                        }
+                    }
+                }
+                reset();
+            }
+            if (group_end) {
+                pos = 0;
+                ++gl;
+            }
         }
-#pragma unroll
-        for (int m = 0; m < M; ++m)
-#pragma unroll
-            for (int t = 0; t < T; ++t) acc[m][t] = fmaf((float)sc[t], part[m][t], acc[m][t]);
+    };
+
+    // One round covers K <= 32 * U * WAVES; larger K walks several rounds,
+    // each issuing its loads right before it consumes them.
+    for (int r = 0; r < rounds; ++r) {
+        Buf b;
+        issue(r, b);
+        consume(r, b);
     }
 
     // Lanes c, c+16, c+32, c+48 hold the same columns: combine over kg.
@@ -124,52 +268,52 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(
     for (int m = 0; m < M; ++m)
 #pragma unroll
         for (int t = 0; t < T; ++t) {
-            float v = acc[m][t];
+            float v = y[m][t];
             v += __shfl_xor(v, 16);
             v += __shfl_xor(v, 32);
-            acc[m][t] = v;
+            y[m][t] = v;
         }
-
-    __shared__ float red[kGemvWaves][M][PW];
+    __syncthreads();   // staging storage becomes the reduction buffer
     if (kg == 0) {
 #pragma unroll
         for (int m = 0; m < M; ++m)
 #pragma unroll
-            for (int t = 0; t < T; ++t) red[wave][m][c + 16 * t] = acc[m][t];
+            for (int t = 0; t < T; ++t) sm.red[wave][m][c + 16 * t] = y[m][t];
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < M * PW; i += kGemvThreads) {
+    for (int i = tid; i < M * PW; i += NT) {
         const int m = i / PW, col = i % PW;
         const int n = p * PW + col;
         if (n < N) {
             float v = 0.f;
 #pragma unroll
-            for (int w = 0; w < kGemvWaves; ++w) v += red[w][m][col];
+            for (int w = 0; w < WAVES; ++w) v += sm.red[w][m][col];
             C[(int64_t)m * N + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
         }
     }
+}
+
+template <int BITS, int M>
+int launch_m(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, hipStream_t s) {
+    constexpr int WAVES = M == 1 ? 16 : 8;
+    constexpr int U = 8;
+    return launch(gemv_kernel<BITS, M, WAVES, U>, dim3((unsigned)L.np), dim3(WAVES * 64), 0, s,
+                  A, pk, C, (int)L.K, (int)L.N, L.group, L.s_off, L.z_off, (int)L.na, (int)L.ng);
 }
 
 template <int BITS>
 int launch_bits(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 hipStream_t s) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    dim3 grid((unsigned)L.np), block(kGemvThreads);
-    int K = (int)L.K, N = (int)L.N, G = L.group, na = (int)L.na, ng = (int)L.ng;
     switch (M) {
-#define TF_GEMV_CASE(MM)                                                                        \
-    case MM:                                                                                    \
-        return launch(gemv_kernel<BITS, MM>, grid, block, 0, s, A, pk, C, K, N, G, L.s_off,     \
-                      L.z_off, na, ng);
-        TF_GEMV_CASE(1)
-        TF_GEMV_CASE(2)
-        TF_GEMV_CASE(3)
-        TF_GEMV_CASE(4)
-        TF_GEMV_CASE(5)
-        TF_GEMV_CASE(6)
-        TF_GEMV_CASE(7)
-        TF_GEMV_CASE(8)
-#undef TF_GEMV_CASE
+        case 1: return launch_m<BITS, 1>(L, A, pk, C, s);
+        case 2: return launch_m<BITS, 2>(L, A, pk, C, s);
+        case 3: return launch_m<BITS, 3>(L, A, pk, C, s);
+        case 4: return launch_m<BITS, 4>(L, A, pk, C, s);
+        case 5: return launch_m<BITS, 5>(L, A, pk, C, s);
+        case 6: return launch_m<BITS, 6>(L, A, pk, C, s);
+        case 7: return launch_m<BITS, 7>(L, A, pk, C, s);
+        case 8: return launch_m<BITS, 8>(L, A, pk, C, s);
     }
     return TF_ERR_ARG;
 }

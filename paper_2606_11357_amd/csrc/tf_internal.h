@@ -100,6 +100,7 @@ inline int launch(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t shmem,
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ half2_t as_h2(uint32_t v) { return __builtin_bit_cast(half2_t, v); }
 __device__ __forceinline__ uint32_t as_u32(half2_t v) { return __builtin_bit_cast(uint32_t, v); }
@@ -114,6 +115,18 @@ __device__ __forceinline__ void w4_code_pairs(uint32_t w, uint32_t out[4]) {
     out[1] = ((w >> 4) & 0x000F000Fu) | kMagic2;
     out[2] = ((w >> 8) & 0x000F000Fu) | kMagic2;
     out[3] = ((w >> 12) & 0x000F000Fu) | kMagic2;
+}
+
+// Cheaper variant for sums: the odd pairs are read without a shift, as
+// (1024 + 16 q[k], 1024 + 16 q[k+1]) (nibble in bits 4..7 of each half, still
+// an exact fp16 integer).  out[0], out[2]: rows (0,1), (4,5) as 1024 + q;
+// out[1], out[3]: rows (2,3), (6,7) as 1024 + 16 q.
+__device__ __forceinline__ void w4_code_pairs_x16(uint32_t w, uint32_t out[4]) {
+    const uint32_t w8 = w >> 8;
+    out[0] = (w & 0x000F000Fu) | kMagic2;
+    out[1] = (w & 0x00F000F0u) | kMagic2;
+    out[2] = (w8 & 0x000F000Fu) | kMagic2;
+    out[3] = (w8 & 0x00F000F0u) | kMagic2;
 }
 
 // Unpack one 8-bit dword (rows r..r+3, lowest byte first) -> two half2 pairs
