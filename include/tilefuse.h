@@ -101,17 +101,27 @@ int tf_pack_w8(const uint8_t* qweight, const uint8_t* zeros, const uint16_t* sca
                int64_t K, int64_t N, int group, void* packed, void* stream);
 
 /*
- * Workspace needed by the GEMM entry points for this problem, in bytes
- * (0 when none is needed).  Negative tf_status on bad arguments.
+ * Workspace the matmul entry points can use for this problem, in bytes (0
+ * when the kernels chosen for it need none).  Negative tf_status on bad
+ * arguments.  The workspace holds per-K-slice partial sums and arrival
+ * counters; it lets the decode GEMV split K over many short workgroups.
+ *
+ * Contract for every `workspace` argument below:
+ *  - NULL selects kernels that need none (workspace_bytes is then ignored);
+ *  - otherwise it is a device buffer of at least tf_workspace_bytes(...)
+ *    bytes, 16-byte aligned and ZERO-FILLED before its first use; each call
+ *    returns the arrival counters it used to zero, so the same buffer serves
+ *    any later call (of any shape it is large enough for) without clearing;
+ *  - calls that may run concurrently must not share one workspace.
  */
-int64_t tf_gemm_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group);
+int64_t tf_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group);
 
 /*
  * Prefill GEMM (Section 2.1: M grows with the prompt length):
  *   C_f16[M, N] = A_f16[M, K] x dequant(packed)[K, N], fp32 accumulate, RNE.
- * Any M >= 1.  workspace may be NULL when tf_gemm_workspace_bytes is 0.
- * The dequantized fp16 weight fed to the matrix cores is RNE(s * (q - z)),
- * rounded once.
+ * Any M >= 1 (M <= TF_GEMV_MAX_M runs the GEMV kernels).  The dequantized
+ * fp16 weight fed to the matrix cores is RNE(s * (q - z)), rounded once.
+ * workspace: see tf_workspace_bytes.
  */
 int tf_w4a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,
                   int64_t M, int64_t K, int64_t N, int group,
@@ -124,11 +134,17 @@ int tf_w8a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,
  * Decode GEMV (Section 2.1: batch-1 generation turns linear layers into
  * matrix-vector products), 1 <= M <= TF_GEMV_MAX_M rows of A.
  * Same operands and result as the GEMM; vector ALU only, fp32 accumulate.
+ * With a workspace (see tf_workspace_bytes) K is split over many
+ * workgroups and the slices are added in a fixed order, so for a given
+ * shape and workspace choice the result is bitwise identical run to run
+ * (with and without a workspace the fp32 summation order differs).
  */
 int tf_w4a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,
-                  int64_t M, int64_t K, int64_t N, int group, void* stream);
+                  int64_t M, int64_t K, int64_t N, int group,
+                  void* workspace, size_t workspace_bytes, void* stream);
 int tf_w8a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,
-                  int64_t M, int64_t K, int64_t N, int group, void* stream);
+                  int64_t M, int64_t K, int64_t N, int group,
+                  void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Debug / test exports.  They read the packed buffer through the same device

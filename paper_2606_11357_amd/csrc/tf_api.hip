@@ -17,6 +17,11 @@ int check_weight(int bits, int64_t K, int64_t N, int group) {
     return TF_OK;
 }
 
+// Bytes of workspace the matmul kernels of this problem can use.
+int64_t workspace_bytes(const Layout& L, int64_t M) {
+    return M <= TF_GEMV_MAX_M ? tf::gemv_workspace_bytes(L, M) : tf::gemm_workspace_bytes(L, M);
+}
+
 int check_matmul(int bits, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                  int64_t K, int64_t N, int group) {
     if (!A || !packed || !C) return TF_ERR_NULL;
@@ -27,27 +32,36 @@ int check_matmul(int bits, const uint16_t* A, const void* packed, uint16_t* C, i
     return TF_OK;
 }
 
+// Workspace rules shared by the matmul entry points: NULL selects the
+// single-pass kernels; otherwise it must be large enough and aligned.
+int check_workspace(const Layout& L, int64_t M, const void* ws, size_t ws_bytes) {
+    if (!ws) return TF_OK;
+    if ((int64_t)ws_bytes < workspace_bytes(L, M)) return TF_ERR_ARG;
+    if (misaligned(ws)) return TF_ERR_ALIGN;
+    return TF_OK;
+}
+
 int gemm_entry(int bits, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                int64_t K, int64_t N, int group, void* ws, size_t ws_bytes, void* stream) {
     int rc = check_matmul(bits, A, packed, C, M, K, N, group);
     if (rc) return rc;
     Layout L = tf::make_layout(bits, K, N, group);
-    int64_t need = tf::gemm_workspace_bytes(L, M);
-    if ((int64_t)ws_bytes < need) return TF_ERR_ARG;
-    if (need > 0 && !ws) return TF_ERR_NULL;
-    if (need > 0 && misaligned(ws)) return TF_ERR_ALIGN;
+    rc = check_workspace(L, M, ws, ws_bytes);
+    if (rc) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (M <= TF_GEMV_MAX_M) return tf::launch_gemv(L, A, packed, C, M, s);
+    if (M <= TF_GEMV_MAX_M) return tf::launch_gemv(L, A, packed, C, M, ws, s);
     return tf::launch_gemm(L, A, packed, C, M, ws, ws_bytes, s);
 }
 
 int gemv_entry(int bits, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
-               int64_t K, int64_t N, int group, void* stream) {
+               int64_t K, int64_t N, int group, void* ws, size_t ws_bytes, void* stream) {
     int rc = check_matmul(bits, A, packed, C, M, K, N, group);
     if (rc) return rc;
     if (M > TF_GEMV_MAX_M) return TF_ERR_ARG;
     Layout L = tf::make_layout(bits, K, N, group);
-    return tf::launch_gemv(L, A, packed, C, M, static_cast<hipStream_t>(stream));
+    rc = check_workspace(L, M, ws, ws_bytes);
+    if (rc) return rc;
+    return tf::launch_gemv(L, A, packed, C, M, ws, static_cast<hipStream_t>(stream));
 }
 
 }  // namespace
@@ -97,11 +111,11 @@ int tf_pack_w8(const uint8_t* qweight, const uint8_t* zeros, const uint16_t* sca
                               static_cast<hipStream_t>(stream));
 }
 
-int64_t tf_gemm_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group) {
+int64_t tf_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group) {
     int rc = check_weight(bits, K, N, group);
     if (rc) return rc;
     if (M < 1 || M > TF_MAX_M) return TF_ERR_SHAPE;
-    return tf::gemm_workspace_bytes(tf::make_layout(bits, K, N, group), M);
+    return workspace_bytes(tf::make_layout(bits, K, N, group), M);
 }
 
 int tf_w4a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
@@ -117,13 +131,15 @@ int tf_w8a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, in
 }
 
 int tf_w4a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
-                  int64_t K, int64_t N, int group, void* stream) {
-    return gemv_entry(4, A_f16, packed, C_f16, M, K, N, group, stream);
+                  int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
+                  void* stream) {
+    return gemv_entry(4, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream);
 }
 
 int tf_w8a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
-                  int64_t K, int64_t N, int group, void* stream) {
-    return gemv_entry(8, A_f16, packed, C_f16, M, K, N, group, stream);
+                  int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
+                  void* stream) {
+    return gemv_entry(8, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream);
 }
 
 int tf_unpack(int bits, const void* packed, int64_t K, int64_t N, int group, uint8_t* q_out,

@@ -6,12 +6,12 @@
 // Mapping (the GPU form of the principle of Section 4.4: every compute unit
 // streams its own weight slice, the activations are shared, each workgroup
 // owns distinct outputs and no partial sum leaves it):
-//  - one workgroup per panel of PW output columns, all of K;
-//  - K is walked in segments of KSEG rows; per segment every wave issues the
-//    loads of all its U atoms at once (one 16-byte load per lane per atom)
-//    and the loads of the next segment before it computes the current one,
-//    so the whole weight stream is in flight early;
-//  - the segment's activations and metadata are staged once in LDS;
+//  - a workgroup owns a panel of PW output columns and all of K, or, when the
+//    panels alone are too few to fill the chip and a workspace is given, one
+//    slice of K;
+//  - every wave first loads its slice of x and its groups' metadata, then all
+//    of its U weight atoms (one 16-byte load per lane per atom), and consumes
+//    the atoms in arrival order; x and metadata sit in wave-private LDS;
 //  - a lane owns T columns x 8 rows of an atom: one 16-byte activation slice
 //    per row of A feeds its T columns (the widening idea of Section 4.3: one
 //    activation fragment reused across many outputs).
@@ -23,8 +23,12 @@
 //  - M >= 4: each weight is dequantized once to fp16 with the GEMM's code,
 //    RNE(s (q - z)), and dotted with all M rows of x.
 // All sums are fp32.  Lanes sharing a column combine by cross-lane shuffles,
-// the waves through LDS, in a fixed order: results are bitwise reproducible.
+// the waves through LDS; K-slices through a workspace, added by the last
+// slice to finish in slice order.  Every order is fixed, so results are
+// bitwise reproducible.
 #include "tf_internal.h"
+
+#include <algorithm>
 
 namespace tf {
 namespace {
@@ -49,11 +53,14 @@ struct WaveStage {
     uint64_t z[U * PW / 8];
 };
 
-template <int BITS, int M, int WAVES, int U>
+// APG: atoms per group when known at compile time (4 for G = 128), else 0.
+template <int BITS, int M, int WAVES, int U, int APG>
 __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
-    int K, int N, int group, int64_t s_off, int64_t z_off, int na, int ng) {
+    int K, int N, int group, int64_t s_off, int64_t z_off, int na, int ng, int S, int AS,
+    float* __restrict__ ws_part, uint32_t* __restrict__ ws_cnt) {
     using Cfg = GemvCfg<BITS, M, WAVES, U>;
+    static_assert(APG == 0 || U % APG == 0, "a wave's run must hold whole groups");
     constexpr int T = Cfg::T, PW = Cfg::PW, RA = Cfg::ROUND_ATOMS;
     constexpr bool FACT = Cfg::FACT;
     constexpr int NT = WAVES * 64;
@@ -65,16 +72,20 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     __shared__ __align__(16) Smem sm;
 
     const int p = blockIdx.x;
+    const int split = blockIdx.y;                       // K-slice of this workgroup
+    const int a_begin = split * AS;
+    const int a_end = min(na, a_begin + AS);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar) index math
     const int c = lane & 15, kg = lane >> 4;
-    const int apg = group / kAtomK;
+    const int apg = APG > 0 ? APG : group / kAtomK;
+    const uint32_t magic = magic_reg();
     const u32x4* wpanel = reinterpret_cast<const u32x4*>(packed) + (int64_t)p * na * 64 + lane;
     const uint8_t* spanel = packed + s_off + (int64_t)p * ng * PW * 2;
     const uint8_t* zpanel = packed + z_off + (int64_t)p * ng * PW;
     const int64_t s_last = ((int64_t)ng * PW * 2 - 16);     // last 16-byte slot of the panel's scales
     const int64_t z_last = ((int64_t)ng * PW - 8);
-    const int rounds = (na + RA - 1) / RA;
+    const int rounds = (a_end - a_begin + RA - 1) / RA;
     Stage& st = sm.st[wave];
 
     float y[M][T];
@@ -94,7 +105,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         u32x4 w[U];
     };
     auto issue = [&](int r, Buf& b) {
-        const int a0 = r * RA + wave * U;
+        const int a0 = a_begin + r * RA + wave * U;
         const int k0 = min(a0, na - 1) * kAtomK;
 #pragma unroll
         for (int m = 0; m < M; ++m) {
@@ -110,8 +121,8 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     };
 
     auto consume = [&](int r, Buf& b) {
-        const int a0 = r * RA + wave * U;
-        if (a0 >= na) return;
+        const int a0 = a_begin + r * RA + wave * U;
+        if (a0 >= a_end) return;
         const int g0 = a0 / apg;
         int pos = a0 - g0 * apg;      // atom a0's place inside its group
         int gl = 0;                   // current group, relative to g0
@@ -142,7 +153,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 #pragma unroll
         for (int i = 0; i < U; ++i) {
             const int a = a0 + i;
-            if (a >= na) break;
+            if (a >= a_end) break;
             u32x4 xv[M];
 #pragma unroll
             for (int m = 0; m < M; ++m)
@@ -172,7 +183,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                         y[m][t] = v;
                     }
                 }
-                if (++pos == apg) {
+                if (APG > 0 ? (i + 1) % (APG > 0 ? APG : 1) == 0 : ++pos == apg) {
                     pos = 0;
                     ++gl;
                 }
@@ -182,7 +193,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
             for (int t = 0; t < T; ++t) {
                 uint32_t P[4];
                 if constexpr (BITS == 4) {
-                    w4_code_pairs_x16(wd[t], P);
+                    w4_code_pairs_x16(wd[t], magic, P);
                 } else {
                     w8_code_pairs(wd[2 * t], P);
                     w8_code_pairs(wd[2 * t + 1], P + 2);
@@ -223,8 +234,10 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                 }
             }
             // close the group at its last atom or at the end of this wave's run
-            const bool group_end = ++pos == apg;
-            if (group_end || i == U - 1 || a + 1 == na) {
+            // (with APG known, runs start on group boundaries: see plan_gemv)
+            const bool group_end = APG > 0 ? (i + 1) % (APG > 0 ? APG : 1) == 0 : ++pos == apg;
+            const bool run_end = APG > 0 ? false : (i == U - 1 || a + 1 == a_end);
+            if (group_end || run_end || (APG > 0 && a + 1 == a_end)) {
                 const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
                 const uint8_t* zp = zbytes + gl * PW + c * T;
 #pragma unroll
@@ -281,48 +294,145 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
             for (int t = 0; t < T; ++t) sm.red[wave][m][c + 16 * t] = y[m][t];
     }
     __syncthreads();
+    if (S == 1) {
+        for (int i = tid; i < M * PW; i += NT) {
+            const int m = i / PW, col = i % PW;
+            const int n = p * PW + col;
+            if (n < N) {
+                float v = 0.f;
+#pragma unroll
+                for (int w = 0; w < WAVES; ++w) v += sm.red[w][m][col];
+                C[(int64_t)m * N + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
+            }
+        }
+        return;
+    }
+    // Split K: park this slice's partial sums, and let the last slice of the
+    // panel to arrive add all of them in slice order (fixed order: bitwise
+    // reproducible whichever workgroup comes last) and write the output.
+    // Partials and counters are touched only by agent-scope atomic accesses,
+    // which write through / read past the per-XCD L2; the wait for the
+    // partial stores to complete orders them before the arrival count.  No
+    // device-wide fence is used: on this part it would write back the whole
+    // L2 of the XCD from every workgroup.
+    float* part = ws_part + (int64_t)p * S * M * PW;
+    for (int i = tid; i < M * PW; i += NT) {
+        const int m = i / PW, col = i % PW;
+        float v = 0.f;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) v += sm.red[w][m][col];
+        __hip_atomic_store(&part[split * M * PW + i], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __builtin_amdgcn_s_waitcnt(0);      // this thread's partial stores have completed
+    __syncthreads();
+    __shared__ int last;
+    if (tid == 0)
+        last = __hip_atomic_fetch_add(&ws_cnt[p], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+               (uint32_t)(S - 1);
+    __syncthreads();
+    if (!last) return;
     for (int i = tid; i < M * PW; i += NT) {
         const int m = i / PW, col = i % PW;
         const int n = p * PW + col;
-        if (n < N) {
-            float v = 0.f;
-#pragma unroll
-            for (int w = 0; w < WAVES; ++w) v += sm.red[w][m][col];
-            C[(int64_t)m * N + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
-        }
+        float v = 0.f;
+        for (int s2 = 0; s2 < S; ++s2)
+            v += __hip_atomic_load(&part[s2 * M * PW + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (n < N) C[(int64_t)m * N + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
     }
+    if (tid == 0)   // leave the counter at zero for the next call
+        __hip_atomic_store(&ws_cnt[p], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Launch plan.  A workgroup of WAVES waves owns one panel and one K-slice of
+// AS atoms.  K is split only when the panels alone would leave much of the
+// chip idle (few output columns): splitting costs a partial-sum round trip,
+// which only pays when it adds many more busy compute units.
+struct GemvPlan {
+    int waves, S, AS;
+};
+constexpr int kGemvU = 8, kMaxSplit = 32;
+constexpr int64_t kSplitBelowPanels = 192;   // split K only below this many panels
+constexpr int64_t kTargetWorkgroups = 256;
+
+inline int gemv_waves(int64_t M) { return M == 1 ? 16 : 8; }
+
+inline GemvPlan plan_gemv(const Layout& L, int64_t M) {
+    const int waves = gemv_waves(M);
+    const int64_t ra = (int64_t)waves * kGemvU;
+    const int64_t apg = L.group / kAtomK;
+    int64_t S = 1;
+    if (L.np < kSplitBelowPanels) {
+        S = (kTargetWorkgroups + L.np - 1) / L.np;
+        S = std::min<int64_t>(S, (L.na + ra - 1) / ra);
+        S = std::min<int64_t>(S, kMaxSplit);
+        S = std::max<int64_t>(S, 1);
+    }
+    int64_t AS = (L.na + S - 1) / S;
+    AS = (AS + apg - 1) / apg * apg;     // slices start on group boundaries
+    S = (L.na + AS - 1) / AS;            // no empty slice
+    return {waves, (int)S, (int)AS};
+}
+
+// Workspace layout: arrival counters first, at a fixed place and sized for
+// the largest panel count any shape can have, so every call finds its
+// counters where an earlier call (of any shape) left them at zero; then the
+// per-slice partial sums, which are always written before they are read.
+constexpr int64_t kCounterBytes = (TF_MAX_DIM / 32) * 4;
+
+
+template <int BITS, int M, int APG>
+int launch_g(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, void* ws,
+             hipStream_t s) {
+    constexpr int WAVES = M == 1 ? 16 : 8;
+    const GemvPlan sp = plan_gemv(L, M);
+    const bool split = ws != nullptr && sp.S > 1;
+    uint32_t* cnt = split ? static_cast<uint32_t*>(ws) : nullptr;
+    float* part = split ? reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kCounterBytes) : nullptr;
+    const int S = split ? sp.S : 1;
+    const int AS = split ? sp.AS : (int)L.na;
+    return launch(gemv_kernel<BITS, M, WAVES, kGemvU, APG>, dim3((unsigned)L.np, (unsigned)S),
+                  dim3(WAVES * 64), 0, s, A, pk, C, (int)L.K, (int)L.N, L.group, L.s_off, L.z_off,
+                  (int)L.na, (int)L.ng, S, AS, part, cnt);
 }
 
 template <int BITS, int M>
-int launch_m(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, hipStream_t s) {
-    constexpr int WAVES = M == 1 ? 16 : 8;
-    constexpr int U = 8;
-    return launch(gemv_kernel<BITS, M, WAVES, U>, dim3((unsigned)L.np), dim3(WAVES * 64), 0, s,
-                  A, pk, C, (int)L.K, (int)L.N, L.group, L.s_off, L.z_off, (int)L.na, (int)L.ng);
+int launch_m(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, void* ws,
+             hipStream_t s) {
+    // group 128 (the AWQ default) gets group boundaries fixed at compile time
+    if (L.group == 128) return launch_g<BITS, M, 4>(L, A, pk, C, ws, s);
+    return launch_g<BITS, M, 0>(L, A, pk, C, ws, s);
 }
 
 template <int BITS>
 int launch_bits(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
-                hipStream_t s) {
+                void* ws, hipStream_t s) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
     switch (M) {
-        case 1: return launch_m<BITS, 1>(L, A, pk, C, s);
-        case 2: return launch_m<BITS, 2>(L, A, pk, C, s);
-        case 3: return launch_m<BITS, 3>(L, A, pk, C, s);
-        case 4: return launch_m<BITS, 4>(L, A, pk, C, s);
-        case 5: return launch_m<BITS, 5>(L, A, pk, C, s);
-        case 6: return launch_m<BITS, 6>(L, A, pk, C, s);
-        case 7: return launch_m<BITS, 7>(L, A, pk, C, s);
-        case 8: return launch_m<BITS, 8>(L, A, pk, C, s);
+        case 1: return launch_m<BITS, 1>(L, A, pk, C, ws, s);
+        case 2: return launch_m<BITS, 2>(L, A, pk, C, ws, s);
+        case 3: return launch_m<BITS, 3>(L, A, pk, C, ws, s);
+        case 4: return launch_m<BITS, 4>(L, A, pk, C, ws, s);
+        case 5: return launch_m<BITS, 5>(L, A, pk, C, ws, s);
+        case 6: return launch_m<BITS, 6>(L, A, pk, C, ws, s);
+        case 7: return launch_m<BITS, 7>(L, A, pk, C, ws, s);
+        case 8: return launch_m<BITS, 8>(L, A, pk, C, ws, s);
     }
     return TF_ERR_ARG;
 }
 
 }  // namespace
 
+int64_t gemv_workspace_bytes(const Layout& L, int64_t M) {
+    if (M < 1 || M > TF_GEMV_MAX_M) return 0;
+    const GemvPlan sp = plan_gemv(L, M);
+    if (sp.S <= 1) return 0;
+    return kCounterBytes + align256((int64_t)L.np * sp.S * M * L.pw * 4);
+}
+
 int launch_gemv(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
-                hipStream_t s) {
-    return L.bits == 4 ? launch_bits<4>(L, A, packed, C, M, s) : launch_bits<8>(L, A, packed, C, M, s);
+                void* ws, hipStream_t s) {
+    return L.bits == 4 ? launch_bits<4>(L, A, packed, C, M, ws, s)
+                       : launch_bits<8>(L, A, packed, C, M, ws, s);
 }
 
 }  // namespace tf

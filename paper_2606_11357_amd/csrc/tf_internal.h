@@ -117,16 +117,26 @@ __device__ __forceinline__ void w4_code_pairs(uint32_t w, uint32_t out[4]) {
     out[3] = ((w >> 12) & 0x000F000Fu) | kMagic2;
 }
 
+// kMagic2 held in a register the compiler cannot see through: VOP3
+// instructions cannot carry literal constants on this target, and with both
+// operands literal the compiler splits (w & mask) | magic into two
+// instructions; with the magic in a register it emits one v_and_or_b32.
+__device__ __forceinline__ uint32_t magic_reg() {
+    uint32_t m;
+    asm("v_mov_b32 %0, 0x64006400" : "=v"(m));
+    return m;
+}
+
 // Cheaper variant for sums: the odd pairs are read without a shift, as
 // (1024 + 16 q[k], 1024 + 16 q[k+1]) (nibble in bits 4..7 of each half, still
 // an exact fp16 integer).  out[0], out[2]: rows (0,1), (4,5) as 1024 + q;
-// out[1], out[3]: rows (2,3), (6,7) as 1024 + 16 q.
-__device__ __forceinline__ void w4_code_pairs_x16(uint32_t w, uint32_t out[4]) {
+// out[1], out[3]: rows (2,3), (6,7) as 1024 + 16 q.  `magic` = kMagic2.
+__device__ __forceinline__ void w4_code_pairs_x16(uint32_t w, uint32_t magic, uint32_t out[4]) {
     const uint32_t w8 = w >> 8;
-    out[0] = (w & 0x000F000Fu) | kMagic2;
-    out[1] = (w & 0x00F000F0u) | kMagic2;
-    out[2] = (w8 & 0x000F000Fu) | kMagic2;
-    out[3] = (w8 & 0x00F000F0u) | kMagic2;
+    out[0] = (w & 0x000F000Fu) | magic;
+    out[1] = (w & 0x00F000F0u) | magic;
+    out[2] = (w8 & 0x000F000Fu) | magic;
+    out[3] = (w8 & 0x00F000F0u) | magic;
 }
 
 // Unpack one 8-bit dword (rows r..r+3, lowest byte first) -> two half2 pairs
@@ -185,8 +195,9 @@ int launch_unpack(const Layout& L, const void* packed, uint8_t* q_out, uint8_t* 
                   hipStream_t s);
 int launch_dequant(const Layout& L, const void* packed, int out_dtype, void* w_out,
                    hipStream_t s);
+int64_t gemv_workspace_bytes(const Layout& L, int64_t M);
 int launch_gemv(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
-                hipStream_t s);
+                void* ws, hipStream_t s);
 int64_t gemm_workspace_bytes(const Layout& L, int64_t M);
 int launch_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, size_t ws_bytes, hipStream_t s);

@@ -26,7 +26,7 @@ GEMV_MAX_M = 8
 
 EXPORTS = (
     "tf_layout_version", "tf_status_str", "tf_packed_bytes", "tf_pack_w4", "tf_pack_w8",
-    "tf_gemm_workspace_bytes", "tf_w4a16_gemm", "tf_w8a16_gemm", "tf_w4a16_gemv",
+    "tf_workspace_bytes", "tf_w4a16_gemm", "tf_w8a16_gemm", "tf_w4a16_gemv",
     "tf_w8a16_gemv", "tf_unpack", "tf_dequant",
 )
 
@@ -56,11 +56,11 @@ def load() -> ctypes.CDLL:
         "tf_packed_bytes": (I64, [I, I64, I64, I]),
         "tf_pack_w4": (I, [P, P, P, I64, I64, I, P, P]),
         "tf_pack_w8": (I, [P, P, P, I64, I64, I, P, P]),
-        "tf_gemm_workspace_bytes": (I64, [I, I64, I64, I64, I]),
+        "tf_workspace_bytes": (I64, [I, I64, I64, I64, I]),
         "tf_w4a16_gemm": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_w8a16_gemm": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
-        "tf_w4a16_gemv": (I, [P, P, P, I64, I64, I64, I, P]),
-        "tf_w8a16_gemv": (I, [P, P, P, I64, I64, I64, I, P]),
+        "tf_w4a16_gemv": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
+        "tf_w8a16_gemv": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_unpack": (I, [I, P, I64, I64, I, P, P, P]),
         "tf_dequant": (I, [I, P, I64, I64, I, I, P, P]),
     }
@@ -113,11 +113,31 @@ def packed_bytes(bits: int, K: int, N: int, group: int = 128) -> int:
     return int(n)
 
 
-def gemm_workspace_bytes(bits: int, M: int, K: int, N: int, group: int = 128) -> int:
-    n = load().tf_gemm_workspace_bytes(bits, M, K, N, group)
+def workspace_bytes(bits: int, M: int, K: int, N: int, group: int = 128) -> int:
+    n = load().tf_workspace_bytes(bits, M, K, N, group)
     if n < 0:
-        raise TileFuseError(int(n), "tf_gemm_workspace_bytes")
+        raise TileFuseError(int(n), "tf_workspace_bytes")
     return int(n)
+
+
+_default_ws = {}
+
+
+def default_workspace(device, nbytes: int):
+    """A zero-filled workspace of at least `nbytes`, cached per device.
+
+    Every call returns the workspace's arrival counters to zero, so the cached
+    buffer serves later calls of any shape without clearing; it must not be
+    shared by calls running concurrently on different streams (pass your own
+    workspace for that).
+    """
+    torch = _torch()
+    key = torch.device(device).index if torch.device(device).index is not None else torch.cuda.current_device()
+    buf = _default_ws.get(key)
+    if buf is None or buf.numel() < nbytes:
+        buf = torch.zeros(max(nbytes, 1 << 20), dtype=torch.uint8, device=device)
+        _default_ws[key] = buf
+    return buf
 
 
 def pack_w4(qweight, qzeros, scales, K: int, N: int, group: int = 128, out=None):
@@ -142,48 +162,45 @@ def pack_w8(qweight, zeros, scales, K: int, N: int, group: int = 128, out=None):
     return out
 
 
-def _matmul(name, A, packed, K, N, group, out, workspace=None):
+def _matmul(bits, kind, A, packed, K, N, group, out, workspace):
+    """workspace: None -> the cached per-device default, False -> none (single-pass
+    kernels), or a caller tensor (zero-filled before its first use)."""
     torch = _torch()
-    _need_cuda(A, packed, out, workspace)
+    _need_cuda(A, packed, out)
     M = A.shape[0]
     if A.dtype != torch.float16 or A.dim() != 2 or A.shape[1] != K:
         raise ValueError("A must be fp16 [M, K]")
     if out is None:
         out = torch.empty((M, N), dtype=torch.float16, device=A.device)
-    fn = getattr(load(), name)
-    if name.endswith("gemm"):
-        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-        rc = fn(_ptr(A), _ptr(packed), _ptr(out), M, K, N, group, _ptr(workspace), ws_bytes,
-                _stream(A.device))
+    if workspace is None:
+        need = workspace_bytes(bits, M, K, N, group)
+        workspace = default_workspace(A.device, need) if need else False
+    if workspace is False:
+        ws_ptr, ws_bytes = None, 0
     else:
-        rc = fn(_ptr(A), _ptr(packed), _ptr(out), M, K, N, group, _stream(A.device))
+        _need_cuda(workspace)
+        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
+    name = f"tf_w{bits}a16_{kind}"
+    rc = getattr(load(), name)(_ptr(A), _ptr(packed), _ptr(out), M, K, N, group, ws_ptr, ws_bytes,
+                               _stream(A.device))
     _check(rc, name)
     return out
 
 
-def _gemm(bits, A, packed, K, N, group, out, workspace):
-    torch = _torch()
-    if workspace is None:
-        need = gemm_workspace_bytes(bits, A.shape[0], K, N, group)
-        if need:
-            workspace = torch.empty(need, dtype=torch.uint8, device=A.device)
-    return _matmul(f"tf_w{bits}a16_gemm", A, packed, K, N, group, out, workspace)
-
-
 def w4a16_gemm(A, packed, K: int, N: int, group: int = 128, out=None, workspace=None):
-    return _gemm(4, A, packed, K, N, group, out, workspace)
+    return _matmul(4, "gemm", A, packed, K, N, group, out, workspace)
 
 
 def w8a16_gemm(A, packed, K: int, N: int, group: int = 128, out=None, workspace=None):
-    return _gemm(8, A, packed, K, N, group, out, workspace)
+    return _matmul(8, "gemm", A, packed, K, N, group, out, workspace)
 
 
-def w4a16_gemv(A, packed, K: int, N: int, group: int = 128, out=None):
-    return _matmul("tf_w4a16_gemv", A, packed, K, N, group, out)
+def w4a16_gemv(A, packed, K: int, N: int, group: int = 128, out=None, workspace=None):
+    return _matmul(4, "gemv", A, packed, K, N, group, out, workspace)
 
 
-def w8a16_gemv(A, packed, K: int, N: int, group: int = 128, out=None):
-    return _matmul("tf_w8a16_gemv", A, packed, K, N, group, out)
+def w8a16_gemv(A, packed, K: int, N: int, group: int = 128, out=None, workspace=None):
+    return _matmul(8, "gemv", A, packed, K, N, group, out, workspace)
 
 
 def unpack(bits: int, packed, K: int, N: int, group: int = 128):

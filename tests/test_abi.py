@@ -98,7 +98,7 @@ MATMUL_OK = dict(A=P, packed=P, C=P, M=4, K=256, N=64, G=128)
 def _gemv(lib, bits, **kw):
     a = {**MATMUL_OK, **kw}
     fn = lib.tf_w4a16_gemv if bits == 4 else lib.tf_w8a16_gemv
-    return fn(a["A"], a["packed"], a["C"], a["M"], a["K"], a["N"], a["G"], NULL)
+    return fn(a["A"], a["packed"], a["C"], a["M"], a["K"], a["N"], a["G"], NULL, 0, NULL)
 
 
 def _gemm(lib, bits, ws=NULL, ws_bytes=0, **kw):
@@ -137,12 +137,28 @@ def test_gemv_rejects_large_m(lib, bits):
     assert _gemv(lib, bits, M=4096) == tfb.TF_ERR_ARG
 
 
-def test_gemm_workspace_query(lib):
-    for bits, M, K, N in [(4, 2048, 4096, 14336), (8, 512, 4096, 4096), (4, 16, 2048, 2048)]:
-        n = lib.tf_gemm_workspace_bytes(bits, M, K, N, 128)
-        assert n >= 0
-    assert lib.tf_gemm_workspace_bytes(4, 0, 256, 64, 128) == tfb.TF_ERR_SHAPE
-    assert lib.tf_gemm_workspace_bytes(4, 16, 256, 64, 100) == tfb.TF_ERR_GROUP
+def test_workspace_query(lib):
+    for bits, M, K, N in [(4, 2048, 4096, 14336), (8, 512, 4096, 4096), (4, 16, 2048, 2048),
+                          (4, 1, 4096, 14336), (8, 8, 4096, 4096)]:
+        n = lib.tf_workspace_bytes(bits, M, K, N, 128)
+        assert n >= 0 and n % 256 == 0
+    # many panels: one workgroup per panel fills the chip, no K split
+    assert lib.tf_workspace_bytes(4, 1, 4096, 14336, 128) == 0
+    # few panels and long K (down-projection): K is split, partial sums + counters
+    assert lib.tf_workspace_bytes(4, 1, 14336, 4096, 128) > 64 * 64 * 4
+    assert lib.tf_workspace_bytes(4, 0, 256, 64, 128) == tfb.TF_ERR_SHAPE
+    assert lib.tf_workspace_bytes(4, 16, 256, 64, 100) == tfb.TF_ERR_GROUP
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_workspace_rejects(lib, bits):
+    need = lib.tf_workspace_bytes(bits, 1, 14336, 4096, 128)
+    assert need > 0
+    fn = lib.tf_w4a16_gemv if bits == 4 else lib.tf_w8a16_gemv
+    assert fn(P, P, P, 1, 14336, 4096, 128, P, need - 16, NULL) == tfb.TF_ERR_ARG
+    assert fn(P, P, P, 1, 14336, 4096, 128, P_ODD, need, NULL) == tfb.TF_ERR_ALIGN
+    fn = lib.tf_w4a16_gemm if bits == 4 else lib.tf_w8a16_gemm
+    assert fn(P, P, P, 1, 14336, 4096, 128, P, need - 16, NULL) == tfb.TF_ERR_ARG
 
 
 def test_pack_rejects(lib):

@@ -56,13 +56,13 @@ def check_guard(buf):
     assert np.all(g == -7.0), "write outside the output"
 
 
-def run(tf, kind, d, packed, x=None):
+def run(tf, kind, d, packed, x=None, workspace=None):
     K, N, G = d["K"], d["N"], d["group"]
     x = d["x"] if x is None else x
     M = x.shape[0]
     buf, out = guarded_out(M, N)
     fn = getattr(tf, f"w{d['bits']}a16_{kind}")
-    fn(dev(x), packed, K, N, G, out=out)
+    fn(dev(x), packed, K, N, G, out=out, workspace=workspace)
     torch.cuda.synchronize()
     check_guard(buf)
     return out.cpu().numpy()
@@ -206,6 +206,38 @@ def test_closed_form(tf):
         for kind, M in (("gemv", 3), ("gemm", 40)):
             got = run(tf, kind, d, packed, x=np.ones((M, K), dtype=np.float16))
             np.testing.assert_array_equal(got, np.full((M, N), K * 7 / 64, dtype=np.float16))
+
+
+@pytest.mark.parametrize("bits,M,K,N", [(4, 1, 4096, 14336), (4, 1, 14336, 4096), (8, 1, 14336, 4096),
+                                        (4, 3, 8192, 1000), (8, 8, 8192, 520), (4, 5, 32768, 136),
+                                        (4, 2, 256, 64), (8, 1, 4096, 4096)])
+def test_gemv_workspace_modes(tf, bits, M, K, N):
+    """Split-K (workspace) and single-pass (no workspace) kernels both meet the
+    bar, and a workspace can be reused at once."""
+    d = make_inputs(bits, M, K, N, seed=M * 11 + N)
+    packed = pack(tf, d)
+    want = ref(d)
+    need = tf.workspace_bytes(bits, M, K, N)
+    ws = torch.zeros(need + 256, dtype=torch.uint8, device="cuda") if need else False
+    a = run(tf, "gemv", d, packed, workspace=ws)
+    b = run(tf, "gemv", d, packed, workspace=ws)
+    np.testing.assert_array_equal(a.view(np.uint16), b.view(np.uint16))
+    c = run(tf, "gemv", d, packed, workspace=False)
+    assert_parity(a, want, "gemv with workspace")
+    assert_parity(c, want, "gemv without workspace")
+
+
+def test_workspace_shared_across_shapes(tf):
+    """One workspace serves a sequence of different problems (different M,
+    bits, panel counts and K-splits) without clearing in between."""
+    cases = [(8, 2, 14336, 4096), (4, 4, 8192, 2048), (4, 1, 14336, 4096), (8, 8, 8192, 520),
+             (4, 7, 4096, 3000), (4, 1, 4096, 14336), (8, 1, 2048, 64), (4, 1, 14336, 4096)]
+    need = max(tf.workspace_bytes(b, m, k, n) for b, m, k, n in cases)
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    for i, (bits, M, K, N) in enumerate(cases):
+        d = make_inputs(bits, M, K, N, seed=100 + i)
+        assert_parity(run(tf, "gemv", d, pack(tf, d), workspace=ws), ref(d),
+                      f"shared workspace, case {i}: W{bits} {M}x{K}x{N}")
 
 
 @pytest.mark.parametrize("kind,M", [("gemv", 1), ("gemv", 8), ("gemm", 300)])
