@@ -32,8 +32,16 @@ FLAGS = [
 ]
 
 
+# Per-source extra flags.  The GEMM keeps its MFMA accumulators in ordinary
+# VGPRs: with the default AGPR form the register allocator rotates the 128
+# loop-carried accumulators through AGPR copies every K step.
+EXTRA = {
+    "tf_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
+
 def _compile(src: str, obj: str) -> None:
-    cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {os.path.basename(src)}:\n{r.stderr}")

@@ -170,7 +170,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                     const half2_t s2 = as_h2(sb | (sb << 16));
                     half8_t w8;
                     if constexpr (BITS == 4)
-                        w8 = dq_w4_dword(wd[t], neg_zero_pair(zp[t]), s2);
+                        w8 = dq_w4_dword(wd[t], magic, neg_zero_pair(zp[t]), s2);
                     else
                         w8 = dq_w8_dwords(wd[2 * t], wd[2 * t + 1], neg_zero_pair(zp[t]), s2);
                     const half2_t w2[4] = {{w8[0], w8[1]}, {w8[2], w8[3]}, {w8[4], w8[5]}, {w8[6], w8[7]}};

@@ -108,14 +108,6 @@ __device__ __forceinline__ uint32_t as_u32(half2_t v) { return __builtin_bit_cas
 // fp16 bit patterns: 0x6400 | v is exactly 1024 + v for 0 <= v < 1024.
 constexpr uint32_t kMagic2 = 0x64006400u;
 
-// Unpack (Section 4.3): one packed 4-bit dword -> four half2 K-pairs holding
-// (1024 + q[k], 1024 + q[k+1]) for row offsets (0,1), (2,3), (4,5), (6,7).
-__device__ __forceinline__ void w4_code_pairs(uint32_t w, uint32_t out[4]) {
-    out[0] = (w & 0x000F000Fu) | kMagic2;
-    out[1] = ((w >> 4) & 0x000F000Fu) | kMagic2;
-    out[2] = ((w >> 8) & 0x000F000Fu) | kMagic2;
-    out[3] = ((w >> 12) & 0x000F000Fu) | kMagic2;
-}
 
 // kMagic2 held in a register the compiler cannot see through: VOP3
 // instructions cannot carry literal constants on this target, and with both
@@ -125,6 +117,16 @@ __device__ __forceinline__ uint32_t magic_reg() {
     uint32_t m;
     asm("v_mov_b32 %0, 0x64006400" : "=v"(m));
     return m;
+}
+
+// Unpack (Section 4.3): one packed 4-bit dword -> four half2 K-pairs holding
+// (1024 + q[k], 1024 + q[k+1]) for row offsets (0,1), (2,3), (4,5), (6,7).
+// `magic` = kMagic2 (pass magic_reg()).
+__device__ __forceinline__ void w4_code_pairs(uint32_t w, uint32_t magic, uint32_t out[4]) {
+    out[0] = (w & 0x000F000Fu) | magic;
+    out[1] = ((w >> 4) & 0x000F000Fu) | magic;
+    out[2] = ((w >> 8) & 0x000F000Fu) | magic;
+    out[3] = ((w >> 12) & 0x000F000Fu) | magic;
 }
 
 // Cheaper variant for sums: the odd pairs are read without a shift, as
@@ -163,9 +165,9 @@ __device__ __forceinline__ half2_t dq_pair(uint32_t codes, uint32_t negz2, half2
 }
 
 // Eight dequantized fp16 weights (one MFMA B operand) from one 4-bit dword.
-__device__ __forceinline__ half8_t dq_w4_dword(uint32_t w, uint32_t negz2, half2_t s2) {
+__device__ __forceinline__ half8_t dq_w4_dword(uint32_t w, uint32_t magic, uint32_t negz2, half2_t s2) {
     uint32_t c[4];
-    w4_code_pairs(w, c);
+    w4_code_pairs(w, magic, c);
     half2_t p0 = dq_pair(c[0], negz2, s2), p1 = dq_pair(c[1], negz2, s2);
     half2_t p2 = dq_pair(c[2], negz2, s2), p3 = dq_pair(c[3], negz2, s2);
     return half8_t{p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};

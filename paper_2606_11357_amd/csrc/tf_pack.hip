@@ -107,7 +107,7 @@ __global__ void unpack_weights(int bits, const uint32_t* __restrict__ wreg, uint
     uint32_t w = wreg[d];
     if (bits == 4) {
         uint32_t cp[4];
-        w4_code_pairs(w, cp);
+        w4_code_pairs(w, magic_reg(), cp);
         for (int pr = 0; pr < 4; ++pr) {
             for (int h = 0; h < 2; ++h) {
                 CodePos pos = w4_pos(p, a, lane, t, 2 * pr + h);
@@ -167,8 +167,9 @@ __global__ void dequant_weights(int bits, const uint8_t* __restrict__ packed, in
     uint32_t codes[4];
     if (bits == 4) {
         uint32_t w = atomw[t];
-        w8 = dq_w4_dword(w, neg_zero_pair(z), as_h2(sbits | ((uint32_t)sbits << 16)));
-        w4_code_pairs(w, codes);
+        const uint32_t magic = magic_reg();
+        w8 = dq_w4_dword(w, magic, neg_zero_pair(z), as_h2(sbits | ((uint32_t)sbits << 16)));
+        w4_code_pairs(w, magic, codes);
     } else {
         uint32_t w0 = atomw[2 * t], w1 = atomw[2 * t + 1];
         w8 = dq_w8_dwords(w0, w1, neg_zero_pair(z), as_h2(sbits | ((uint32_t)sbits << 16)));
