@@ -2,17 +2,20 @@
 //   C[M, N] = A[M, K] x dequant(packed)[K, N], fp16 MFMA, fp32 accumulate.
 //
 // Workgroup tile BM x BN = 128 x 256, four waves side by side along N; each
-// wave owns 128 rows x 64 columns.  K is walked in steps of BK = 32 rows.
-//  - A (fp16) goes global -> registers -> LDS, double buffered and XOR
-//    swizzled so the MFMA operand reads are bank-conflict free; the next
-//    step's A is in flight while the current one is multiplied, and there is
+// wave owns 128 rows x 64 columns (one 4-bit panel or two 8-bit panels).
+// K is walked in chunks of 128 rows = 4 steps of 32 rows (one packed atom per
+// panel per step).
+//  - B never exists as fp16 in memory: each wave loads the packed atoms of its
+//    own columns, unpacks and dequantizes them (Eq. 2, rounded once) straight
+//    into the register layout of the v_mfma_f32_16x16x32_f16 B operand, and
+//    reuses every dequantized operand across its 8 row sub-tiles (Sections
+//    4.1.1 and 4.3: dequantize a weight tile once, reuse it for every
+//    activation row).  The next chunk's atoms and metadata are loaded a whole
+//    chunk ahead; the group constants are formed once per chunk.
+//  - A (fp16) goes global -> registers -> LDS through three XOR-swizzled LDS
+//    buffers: the loads for step s+2 leave while step s is multiplied and are
+//    written to LDS one step later, so each load has more than a step to land;
 //    one barrier per step.
-//  - B never exists as fp16 in memory: each wave loads the packed atoms of
-//    its own 64 columns (one 16-byte load per lane per 32 rows), unpacks and
-//    dequantizes them (Eq. 2, rounded once) straight into the register layout
-//    of the v_mfma_f32_16x16x32_f16 B operand, and reuses every dequantized
-//    operand across its 8 row sub-tiles (Sections 4.1.1 and 4.3: dequantize a
-//    weight tile once, reuse it for every activation row).
 //  - Tiles are numbered so that each XCD (workgroups are dealt round-robin
 //    over the 8 XCDs) works on a contiguous band of tiles sharing rows of A,
 //    which then stay in that XCD's L2.
@@ -22,47 +25,44 @@ namespace tf {
 namespace {
 
 constexpr int kBM = 128, kBN = 256, kBK = 32;
-constexpr int kSub = kBK / kAtomK;     // 32-row sub-steps per step
+// Steps per chunk (128 rows of K); also the size of the packed-atom ring.
+template <int BITS>
+constexpr int chunk_steps() { return 4; }
 constexpr int kGemmThreads = 256;
 constexpr int kXcds = 8;
+constexpr int kABufs = 3;
 
-// LDS position (in 16-byte chunks) of chunk `ch` of A row `row` (kBK halves
-// = kChunks chunks per row).  The XOR with row bits spreads the 16 lanes of
-// one ds_read_b128 (16 rows, same chunk) over distinct bank groups of the
-// 64-bank LDS: rows 4 apart are 64 chunks (one bank cycle) apart.
-constexpr int kChunks = kBK / 8;
-__device__ __forceinline__ int a_slot(int row, int ch) {
-    return kChunks == 8 ? row * 8 + (ch ^ ((row >> 1) & 7)) : row * 4 + (ch ^ ((row >> 2) & 3));
-}
+// LDS slot (16-byte chunks) of chunk `ch` (0..3) of A row `row`: rows are 64
+// bytes; the XOR with row bits 2..3 sends the 16 lanes of one ds_read_b128
+// (16 consecutive rows, same chunk) to 16 distinct 4-bank groups of the
+// 64-bank LDS.
+__device__ __forceinline__ int a_slot(int row, int ch) { return row * 4 + (ch ^ ((row >> 2) & 3)); }
 
-template <int BITS>
-struct GemmCfg {
-    static constexpr int PW = BITS == 4 ? 64 : 32;
-    static constexpr int T = PW / 16;                 // columns per lane per atom
-    static constexpr int PANELS = 64 / PW;            // panels per wave (64 columns)
-    static constexpr int ATOMS = PANELS * (kBK / kAtomK);   // atom loads per wave per step
-};
-
-template <int BITS>
+// MPC: metadata groups per chunk (1 when a group spans the whole chunk, else
+// chunk rows / group); the group of step j is j / (chunk steps / MPC).
+template <int BITS, int MPC>
 __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
-    int M, int K, int N, int group, int gshift, int64_t s_off, int64_t z_off, int na, int ng,
-    int np, int tiles_m, int tiles_n) {
-    using Cfg = GemmCfg<BITS>;
-    constexpr int PW = Cfg::PW, T = Cfg::T, PANELS = Cfg::PANELS;
-    __shared__ __align__(16) u32x4 As[2][kBM * kBK / 8];
+    int M, int K, int N, int gshift, int64_t s_off, int64_t z_off, int na, int ng, int np,
+    int tiles_m, int tiles_n) {
+    constexpr int PW = BITS == 4 ? 64 : 32;
+    constexpr int T = PW / 16;                 // columns per lane per atom
+    constexpr int PANELS = 64 / PW;            // panels per wave
+    constexpr int kChunkSteps = chunk_steps<BITS>();
+    constexpr int SPG = kChunkSteps / MPC;     // steps per metadata group
+    __shared__ __align__(16) u32x4 As[kABufs][kBM * kBK / 8];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c = lane & 15, kg = lane >> 4;
     const uint32_t magic = magic_reg();
 
-    // XCD-aware tile order: block b runs on XCD b % 8; give XCD x the x-th
+    // XCD-aware tile order: block b runs on XCD b % 8; XCD x takes the x-th
     // contiguous band of the row-major tile list.
     const int total = tiles_m * tiles_n;
-    const int b = blockIdx.x;
     int tile;
     {
+        const int b = blockIdx.x;
         const int per = total / kXcds, rem = total % kXcds;
         const int x = b % kXcds, i = b / kXcds;
         tile = x * per + min(x, rem) + i;
@@ -77,116 +77,157 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
 #pragma unroll
         for (int t = 0; t < 4; ++t) acc[i][t] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-    // ---- A staging: 128 rows x kBK halves, kAR 16-byte chunks per thread.
-    // Rows past M read row M-1 instead (in bounds; those rows are never stored).
-    constexpr int kAR = kBM * kChunks / kGemmThreads;
-    const uint16_t* arow[kAR];
+    // ---- A: 128 rows x 32 halves per step = 512 chunks, 2 per thread.  Rows
+    // past M read row M-1 instead (in bounds; those rows are never stored).
+    const uint16_t* arow[2];
+    int aslot[2];
 #pragma unroll
-    for (int r = 0; r < kAR; ++r) {
+    for (int r = 0; r < 2; ++r) {
         const int idx = tid + kGemmThreads * r;
-        const int64_t grow = min<int64_t>(row0 + idx / kChunks, (int64_t)M - 1);
-        arow[r] = A + grow * K + (idx % kChunks) * 8;
+        const int64_t grow = min<int64_t>(row0 + (idx >> 2), (int64_t)M - 1);
+        arow[r] = A + grow * K + (idx & 3) * 8;
+        aslot[r] = a_slot(idx >> 2, idx & 3);
     }
-    u32x4 av[kAR];
-    auto load_a = [&](int step) {
+    const int steps = na;                      // one 32-row step per atom
+    auto load_a = [&](int step, u32x4 (&av)[2]) {
+        step = min(step, steps - 1);           // clamped: a repeated valid step, never used
 #pragma unroll
-        for (int r = 0; r < kAR; ++r) av[r] = *reinterpret_cast<const u32x4*>(arow[r] + step * kBK);
+        for (int r = 0; r < 2; ++r) av[r] = *reinterpret_cast<const u32x4*>(arow[r] + step * kBK);
     };
-    auto store_a = [&](int buf) {
+    auto store_a = [&](int buf, const u32x4 (&av)[2]) {
 #pragma unroll
-        for (int r = 0; r < kAR; ++r) {
-            const int idx = tid + kGemmThreads * r;
-            As[buf][a_slot(idx / kChunks, idx % kChunks)] = av[r];
-        }
+        for (int r = 0; r < 2; ++r) As[buf][aslot[r]] = av[r];
     };
 
-    // ---- B: this wave's packed atoms and its columns' metadata.  Panels past
-    // N read the last panel instead (in bounds; their columns are never stored).
+    // ---- B: the wave's packed atoms and its columns' metadata.  Panels past N
+    // read the last panel instead (in bounds; their columns are never stored).
     const u32x4* wp[PANELS];
     const uint8_t* sp[PANELS];
     const uint8_t* zp[PANELS];
-    bool pvalid[PANELS];
+    bool live = false;
 #pragma unroll
     for (int pp = 0; pp < PANELS; ++pp) {
         int64_t panel = col0 / PW + pp;
-        pvalid[pp] = panel < np;
+        live = live || panel < np;
         panel = min<int64_t>(panel, np - 1);
         wp[pp] = reinterpret_cast<const u32x4*>(packed) + panel * na * 64 + lane;
         sp[pp] = packed + s_off + (panel * ng * PW + c * T) * 2;
         zp[pp] = packed + z_off + panel * ng * PW + c * T;
     }
-    // One step's packed weights and raw metadata: [k sub-step][panel].
-    struct BStep {
-        u32x4 w[kSub][PANELS];
-        uint32_t s[kSub][PANELS][(T + 1) / 2];   // T fp16 scales
-        uint32_t z[kSub][PANELS];                // T zero-point bytes (low T bytes)
-    };
-    auto load_b = [&](int step, BStep& bs) {
+    // Packed atoms live in a ring of kChunkSteps slots: the atom of step s sits
+    // in slot s % kChunkSteps, is loaded three steps ahead and is dequantized
+    // one step ahead, while the MFMAs of the step before it run.  Raw metadata
+    // is loaded a chunk ahead; group constants are formed once per group.
+    constexpr int CS = kChunkSteps;
+    const int chunks = steps / CS;            // the launcher requires K % (32 * CS) == 0
+    u32x4 ring[CS][PANELS];
+    auto load_atom = [&](int step, u32x4 (&slot)[PANELS]) {
+        step = min(step, steps - 1);           // clamped: a repeated valid step, never used
 #pragma unroll
-        for (int j = 0; j < kSub; ++j) {
-            const int a = step * kSub + j;
-            const int g = (a * kAtomK) >> gshift;     // group size is a power of two here
+        for (int pp = 0; pp < PANELS; ++pp) slot[pp] = wp[pp][step * 64];
+    };
+    struct Meta {
+        uint32_t s[MPC][PANELS][(T + 1) / 2];   // T fp16 scales per group and panel
+        uint32_t z[MPC][PANELS];                // T zero-point bytes
+    };
+    auto load_meta = [&](int ch, Meta& mt) {
+        ch = min(ch, chunks - 1);
+#pragma unroll
+        for (int m = 0; m < MPC; ++m) {
+            const int g = ((ch * CS + m * SPG) * kAtomK) >> gshift;
 #pragma unroll
             for (int pp = 0; pp < PANELS; ++pp) {
-                bs.w[j][pp] = wp[pp][a * 64];
                 if constexpr (BITS == 4) {
                     const uint2 sv = *reinterpret_cast<const uint2*>(sp[pp] + g * PW * 2);
-                    bs.s[j][pp][0] = sv.x;
-                    bs.s[j][pp][1] = sv.y;
-                    bs.z[j][pp] = *reinterpret_cast<const uint32_t*>(zp[pp] + g * PW);
+                    mt.s[m][pp][0] = sv.x;
+                    mt.s[m][pp][1] = sv.y;
+                    mt.z[m][pp] = *reinterpret_cast<const uint32_t*>(zp[pp] + g * PW);
                 } else {
-                    bs.s[j][pp][0] = *reinterpret_cast<const uint32_t*>(sp[pp] + g * PW * 2);
-                    bs.z[j][pp] = *reinterpret_cast<const uint16_t*>(zp[pp] + g * PW);
+                    mt.s[m][pp][0] = *reinterpret_cast<const uint32_t*>(sp[pp] + g * PW * 2);
+                    mt.z[m][pp] = *reinterpret_cast<const uint16_t*>(zp[pp] + g * PW);
                 }
             }
         }
     };
+    // Group constants: (s, s), -(1024 + z), -(64 + z) for each lane column.
+    struct Consts {
+        half2_t s2[4];
+        uint32_t nz[4], nz64[4];
+    };
+    auto make_consts = [&](const Meta& mt, int m, Consts& k) {
+#pragma unroll
+        for (int pp = 0; pp < PANELS; ++pp)
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                const uint32_t sh = mt.s[m][pp][t / 2] >> (16 * (t & 1));
+                k.s2[pp * T + t] = as_h2(__builtin_amdgcn_perm(sh, sh, 0x01000100u));
+                const uint32_t n = __builtin_amdgcn_perm(0xE4E4E4E4u, mt.z[m][pp], 0x04000400u | (t * 0x00010001u));
+                k.nz[pp * T + t] = n;
+                k.nz64[pp * T + t] = neg_zero64_pair(n);
+            }
+    };
+    auto dequant = [&](const u32x4 (&slot)[PANELS], const Consts& k, half8_t (&bop)[4]) {
+#pragma unroll
+        for (int pp = 0; pp < PANELS; ++pp)
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                const int u = pp * T + t;
+                if constexpr (BITS == 4)
+                    bop[u] = dq_w4_dword(slot[pp][t], magic, k.nz[u], k.nz64[u], k.s2[u]);
+                else
+                    bop[u] = dq_w8_dwords(slot[pp][2 * t], slot[pp][2 * t + 1], k.nz[u], k.s2[u]);
+            }
+    };
 
-    // One step per trip.  The next step's A is loaded into registers at the top
-    // and written to the other LDS buffer after the multiply; the packed B of
-    // the next step was loaded one step earlier and moves into place at the
-    // bottom, while the loads for the step after it go out.  Prefetch indices
-    // are clamped instead of branched on (a clamped load repeats a valid step
-    // whose data is never used).
-    const int steps = na / kSub;     // the launcher requires K % kBK == 0
-    BStep bcur, bnext;
-    load_a(0);
-    load_b(0, bcur);
-    store_a(0);
-    load_b(min(1, steps - 1), bnext);
-    for (int step = 0; step < steps; ++step) {
-        const int buf = step & 1;
-        load_a(min(step + 1, steps - 1));
-        __syncthreads();               // As[buf] complete; As[buf ^ 1] no longer read
+    // Prologue: A for steps 0 and 1 in flight, step 0 in LDS; atoms of steps
+    // 0..2 and metadata of chunks 0 and 1 requested; B operands of step 0.
+    u32x4 ra[2][2];
+    load_a(0, ra[0]);
+    load_a(1, ra[1]);
+    static_assert(CS == 4, "the atom ring needs four slots for its three-step lead");
 #pragma unroll
-        for (int j = 0; j < kSub; ++j) {
-            half8_t bop[4];
+    for (int j = 0; j < 3; ++j) load_atom(j, ring[j]);
+    Meta mcur, mnext;
+    load_meta(0, mcur);
+    load_meta(1, mnext);
+    store_a(0, ra[0]);
+    Consts kc;
+    make_consts(mcur, 0, kc);
+    half8_t bop[4];
+    dequant(ring[0], kc, bop);
+
+    for (int ch = 0; ch < chunks; ++ch) {
 #pragma unroll
-            for (int pp = 0; pp < PANELS; ++pp) {
+        for (int j = 0; j < CS; ++j) {
+            const int step = ch * CS + j;
+            const int buf = step % kABufs;
+            load_a(step + 2, ra[j & 1]);                  // step + 2 has the same parity as step
+            load_atom(step + 3, ring[(j + 3) % CS]);      // that slot held step - 1, used already
+            if (j == CS - 1) {
+                // constants for the first step of the next chunk; the metadata
+                // of the chunk after it is requested
+                mcur = mnext;
+                load_meta(ch + 2, mnext);
+                make_consts(mcur, 0, kc);
+            } else if ((j + 1) % SPG == 0) {
+                make_consts(mcur, (j + 1) / SPG, kc);     // next step starts a new group
+            }
+            __syncthreads();                              // As[buf] written; As[(step + 1) % 3] free
+            half8_t bnext[4];
+            dequant(ring[(j + 1) % CS], kc, bnext);       // B operands of step + 1
+            if (live) {
 #pragma unroll
-                for (int t = 0; t < T; ++t) {
-                    const uint32_t sh = (bcur.s[j][pp][t / 2] >> (16 * (t & 1))) & 0xFFFFu;
-                    const uint32_t sb = pvalid[pp] ? sh : 0u;
-                    const uint32_t zb = pvalid[pp] ? (bcur.z[j][pp] >> (8 * t)) & 0xFFu : 0u;
-                    const half2_t s2 = as_h2(sb | (sb << 16));
-                    if constexpr (BITS == 4)
-                        bop[t] = dq_w4_dword(bcur.w[j][pp][t], magic, neg_zero_pair(zb), s2);
-                    else
-                        bop[pp * T + t] = dq_w8_dwords(bcur.w[j][pp][2 * t], bcur.w[j][pp][2 * t + 1],
-                                                       neg_zero_pair(zb), s2);
+                for (int i = 0; i < 8; ++i) {
+                    const half8_t af = __builtin_bit_cast(half8_t, As[buf][a_slot(16 * i + c, kg)]);
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bop[t], acc[i][t], 0, 0, 0);
                 }
             }
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const half8_t af = __builtin_bit_cast(half8_t, As[buf][a_slot(16 * i + c, kChunks / kSub * j + kg)]);
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bop[t], acc[i][t], 0, 0, 0);
-            }
+            for (int t = 0; t < 4; ++t) bop[t] = bnext[t];
+            store_a((step + 1) % kABufs, ra[(j + 1) & 1]);   // A for step + 1, loaded a step ago
         }
-        store_a(buf ^ 1);
-        bcur = bnext;
-        load_b(min(step + 2, steps - 1), bnext);
     }
 
     // ---- epilogue: lane holds column c of each 16x16 block, rows 4 kg + r
@@ -204,14 +245,15 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
         }
 }
 
-// Generic kernel for the cases the main one leaves out (group size not a
-// power of two): 128 x 128 tiles, 32-row steps, single-buffered.
+// Generic kernel for the cases the main one leaves out (K not a multiple of
+// the chunk or a group size that is not a power of two): 128 x 128 tiles,
+// 32-row steps, single-buffered.
 constexpr int kBM1 = 128, kBN1 = 128, kBK1 = 32;
 
 __device__ __forceinline__ int a_swz1(int row, int chunk) { return row * 4 + (chunk ^ ((row >> 2) & 3)); }
 
 template <int BITS>
-__global__ __launch_bounds__(kGemmThreads) void gemm_kernel_k32(
+__global__ __launch_bounds__(kGemmThreads) void gemm_kernel_generic(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
     int M, int K, int N, int group, int64_t s_off, int64_t z_off, int na, int ng, int np) {
     constexpr int PW = BITS == 4 ? 64 : 32;
@@ -223,6 +265,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_k32(
     const int c = lane & 15, kg = lane >> 4;
     const int64_t row0 = (int64_t)blockIdx.y * kBM1;
     const int64_t col0 = (int64_t)blockIdx.x * kBN1;
+    const uint32_t magic = magic_reg();
 
     float4_t acc[4][4];
 #pragma unroll
@@ -269,10 +312,11 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_k32(
 #pragma unroll
             for (int t = 0; t < T; ++t) {
                 const half2_t s2 = as_h2((uint32_t)sb[t] | ((uint32_t)sb[t] << 16));
+                const uint32_t nz = neg_zero_pair(zb[t]);
                 if constexpr (BITS == 4)
-                    b[t] = dq_w4_dword(wv[t], magic_reg(), neg_zero_pair(zb[t]), s2);
+                    b[t] = dq_w4_dword(wv[t], magic, nz, neg_zero64_pair(nz), s2);
                 else
-                    b[pp * T + t] = dq_w8_dwords(wv[2 * t], wv[2 * t + 1], neg_zero_pair(zb[t]), s2);
+                    b[pp * T + t] = dq_w8_dwords(wv[2 * t], wv[2 * t + 1], nz, s2);
             }
         }
         __syncthreads();
@@ -305,21 +349,32 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_k32(
         }
 }
 
+template <int BITS, int MPC>
+int launch_main(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
+                hipStream_t s) {
+    const int tiles_m = (int)((M + kBM - 1) / kBM);
+    const int tiles_n = (int)((L.N + kBN - 1) / kBN);
+    const int gshift = __builtin_ctz((unsigned)L.group);
+    return launch(gemm_kernel<BITS, MPC>, dim3((unsigned)(tiles_m * tiles_n)), dim3(kGemmThreads), 0, s,
+                  A, pk, C, (int)M, (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na,
+                  (int)L.ng, (int)L.np, tiles_m, tiles_n);
+}
+
 template <int BITS>
 int launch_bits(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
                 hipStream_t s) {
+    constexpr int CS = chunk_steps<BITS>();
+    const int chunk_rows = kBK * CS;
     const bool pow2_group = (L.group & (L.group - 1)) == 0;
-    if (L.K % kBK == 0 && pow2_group) {
-        const int tiles_m = (int)((M + kBM - 1) / kBM);
-        const int tiles_n = (int)((L.N + kBN - 1) / kBN);
-        const int gshift = __builtin_ctz((unsigned)L.group);
-        return launch(gemm_kernel<BITS>, dim3((unsigned)(tiles_m * tiles_n)), dim3(kGemmThreads), 0, s,
-                      A, pk, C, (int)M, (int)L.K, (int)L.N, L.group, gshift, L.s_off, L.z_off,
-                      (int)L.na, (int)L.ng, (int)L.np, tiles_m, tiles_n);
+    if (L.K % chunk_rows == 0 && pow2_group) {
+        const int mpc = L.group >= chunk_rows ? 1 : chunk_rows / L.group;
+        if (mpc == 1) return launch_main<BITS, 1>(L, A, pk, C, M, s);
+        if (mpc == 2) return launch_main<BITS, 2>(L, A, pk, C, M, s);
+        if constexpr (CS >= 4) return launch_main<BITS, 4>(L, A, pk, C, M, s);
     }
     dim3 grid((unsigned)((L.N + kBN1 - 1) / kBN1), (unsigned)((M + kBM1 - 1) / kBM1));
-    return launch(gemm_kernel_k32<BITS>, grid, dim3(kGemmThreads), 0, s, A, pk, C, (int)M, (int)L.K,
-                  (int)L.N, L.group, L.s_off, L.z_off, (int)L.na, (int)L.ng, (int)L.np);
+    return launch(gemm_kernel_generic<BITS>, grid, dim3(kGemmThreads), 0, s, A, pk, C, (int)M,
+                  (int)L.K, (int)L.N, L.group, L.s_off, L.z_off, (int)L.na, (int)L.ng, (int)L.np);
 }
 
 }  // namespace

@@ -169,10 +169,11 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                     const uint32_t sb = sp[t];
                     const half2_t s2 = as_h2(sb | (sb << 16));
                     half8_t w8;
+                    const uint32_t nz = neg_zero_pair(zp[t]);
                     if constexpr (BITS == 4)
-                        w8 = dq_w4_dword(wd[t], magic, neg_zero_pair(zp[t]), s2);
+                        w8 = dq_w4_dword(wd[t], magic, nz, neg_zero64_pair(nz), s2);
                     else
-                        w8 = dq_w8_dwords(wd[2 * t], wd[2 * t + 1], neg_zero_pair(zp[t]), s2);
+                        w8 = dq_w8_dwords(wd[2 * t], wd[2 * t + 1], nz, s2);
                     const half2_t w2[4] = {{w8[0], w8[1]}, {w8[2], w8[3]}, {w8[4], w8[5]}, {w8[6], w8[7]}};
 #pragma unroll
                     for (int m = 0; m < M; ++m) {

@@ -164,12 +164,30 @@ __device__ __forceinline__ half2_t dq_pair(uint32_t codes, uint32_t negz2, half2
     return d * s2;
 }
 
-// Eight dequantized fp16 weights (one MFMA B operand) from one 4-bit dword.
-__device__ __forceinline__ half8_t dq_w4_dword(uint32_t w, uint32_t magic, uint32_t negz2, half2_t s2) {
+// -(64 + z) as an fp16 pair from neg_zero_pair(z): -(1024 + z) + 960, exact.
+__device__ __forceinline__ uint32_t neg_zero64_pair(uint32_t negz2) {
+    const half2_t c960 = {(_Float16)960.0f, (_Float16)960.0f};
+    return as_u32(as_h2(negz2) + c960);
+}
+
+// Eight dequantized fp16 weights (one MFMA B operand) from one 4-bit dword,
+// each RNE(s * (q - z)) rounded once (Eq. 2).  Rows (0,1) and (4,5) are read
+// as 1024 + q and reduced by (1024 + z); rows (2,3) and (6,7) are read without
+// a shift as 1024 + 16 q and reduced by one fused multiply-add,
+// (1024 + 16 q) / 16 - (64 + z), whose exact value q - z is an fp16 integer,
+// so the single rounding of the fma is exact.  Then one multiply by s.
+// negz2 = neg_zero_pair(z), negz64 = neg_zero64_pair(negz2), s2 = (s, s).
+__device__ __forceinline__ half8_t dq_w4_dword(uint32_t w, uint32_t magic, uint32_t negz2,
+                                               uint32_t negz64, half2_t s2) {
+#pragma clang fp contract(off)
     uint32_t c[4];
-    w4_code_pairs(w, magic, c);
-    half2_t p0 = dq_pair(c[0], negz2, s2), p1 = dq_pair(c[1], negz2, s2);
-    half2_t p2 = dq_pair(c[2], negz2, s2), p3 = dq_pair(c[3], negz2, s2);
+    w4_code_pairs_x16(w, magic, c);
+    const half2_t sixteenth = {(_Float16)0.0625f, (_Float16)0.0625f};
+    const half2_t d0 = as_h2(c[0]) + as_h2(negz2);
+    const half2_t d2 = as_h2(c[2]) + as_h2(negz2);
+    const half2_t d1 = __builtin_elementwise_fma(as_h2(c[1]), sixteenth, as_h2(negz64));
+    const half2_t d3 = __builtin_elementwise_fma(as_h2(c[3]), sixteenth, as_h2(negz64));
+    const half2_t p0 = d0 * s2, p1 = d1 * s2, p2 = d2 * s2, p3 = d3 * s2;
     return half8_t{p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};
 }
 

@@ -168,7 +168,8 @@ __global__ void dequant_weights(int bits, const uint8_t* __restrict__ packed, in
     if (bits == 4) {
         uint32_t w = atomw[t];
         const uint32_t magic = magic_reg();
-        w8 = dq_w4_dword(w, magic, neg_zero_pair(z), as_h2(sbits | ((uint32_t)sbits << 16)));
+        const uint32_t nz = neg_zero_pair(z);
+        w8 = dq_w4_dword(w, magic, nz, neg_zero64_pair(nz), as_h2(sbits | ((uint32_t)sbits << 16)));
         w4_code_pairs(w, magic, codes);
     } else {
         uint32_t w0 = atomw[2 * t], w1 = atomw[2 * t + 1];

@@ -156,7 +156,9 @@ def test_gemv_parity_small(tf, bits, M, K, N, G):
 
 GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 200, 64),
                (8, 33, 256, 40, 128), (8, 130, 384, 104, 128), (4, 9, 96, 8, 32),
-               (4, 300, 1024, 520, 128), (8, 64, 128, 4096, 128), (4, 1, 256, 64, 128)]
+               (4, 300, 1024, 520, 128), (8, 64, 128, 4096, 128), (4, 1, 256, 64, 128),
+               (4, 200, 512, 328, 32), (8, 150, 512, 264, 64), (8, 140, 384, 72, 32),
+               (4, 257, 768, 1000, 256), (8, 129, 1024, 200, 1024), (4, 96, 1152, 392, 96)]
 
 
 @pytest.mark.parametrize("bits,M,K,N,G", GEMM_SHAPES)
