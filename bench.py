@@ -14,10 +14,17 @@ Prints ONE JSON line.  `value` is the prefill GEMM throughput in TFLOP/s
 HBM bandwidth (packed codes + fp16 scales + zero-points per launch over its
 average launch time) is reported beside it, each with its roofline fraction.
 Kernel times come from HIP events recorded on the launch stream.
+
+`roofline.traffic` is the HBM bytes per launch measured with rocprofv3
+FETCH_SIZE / WRITE_SIZE counters (scaled by the same counters on a plain copy
+of known size, see --calibrate-copy), recorded in profiles/traffic.json with
+the hash of the kernel source they were taken on; it is null whenever that
+source has changed since.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -25,12 +32,14 @@ import time
 
 import numpy as np
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
 GEMM_SHAPES = [(2048, 4096, 14336), (2048, 14336, 4096)]
 GEMV_SHAPE = (1, 4096, 14336)
 GROUP = 128
 GEMV_REPS = 32
 PEAK_F16_TFLOPS = 2516.6      # 256 CU x 4096 FLOP/clk x 2.4 GHz (dense fp16 MFMA)
 PEAK_HBM_GBS = 8000.0
+COPY_BYTES = 1 << 30
 
 
 def algo_bytes_w4(K, N, G=GROUP):
@@ -39,18 +48,41 @@ def algo_bytes_w4(K, N, G=GROUP):
     return K * N // 2 + (K // G) * N * 2 + (K // G) * N // 2
 
 
+def source_hash(name):
+    """SHA-256 (first 16 hex digits) of a kernel source and the shared header."""
+    h = hashlib.sha256()
+    for f in (name, "tf_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2606_11357_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(kernel_file):
+    """Per-launch HBM bytes from profiles/traffic.json if taken on this source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        rec = json.load(open(path))[kernel_file]
+    except (OSError, KeyError, ValueError):
+        return None
+    if rec.get("source_sha256_16") != source_hash(kernel_file):
+        return None
+    return rec.get("bytes_per_launch")
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
 
 
-def cpu_baseline():
-    """The oracle (fp64, numpy/BLAS) timed on the host on the same prefill
-    GEMM pair (both shapes, full size) and on one decode GEMV."""
+def cpu_baseline(min_seconds=10.0):
+    """The oracle (fp64, numpy/BLAS) timed on the host on whole steps of the
+    same workload: the prefill GEMM pair at full size, then one decode GEMV,
+    repeated until at least `min_seconds` of oracle time have accumulated."""
     import oracle
     from paper_2606_11357_amd.synth import make_inputs
     try:
@@ -58,26 +90,38 @@ def cpu_baseline():
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count()
-    t_gemm, flops = 0.0, 0.0
-    for (M, K, N) in GEMM_SHAPES:
-        d = make_inputs(4, M, K, N, group=GROUP, seed=0)
-        t0 = time.perf_counter()
-        y = oracle.w4a16(d["x"], d["qweight"], d["qzeros"], d["s"], GROUP)
-        t_gemm += time.perf_counter() - t0
-        flops += 2.0 * M * N * K
-        assert np.isfinite(y).all()
-        del d, y
+    gemm_in = [make_inputs(4, M, K, N, group=GROUP, seed=0) for (M, K, N) in GEMM_SHAPES]
     M1, K1, N1 = GEMV_SHAPE
-    d = make_inputs(4, M1, K1, N1, group=GROUP, seed=0)
-    t0 = time.perf_counter()
-    oracle.w4a16(d["x"], d["qweight"], d["qzeros"], d["s"], GROUP)
-    t_gemv = time.perf_counter() - t0
+    gemv_in = make_inputs(4, M1, K1, N1, group=GROUP, seed=0)
+    t_gemm = t_gemv = 0.0
+    reps = 0
+    while t_gemm + t_gemv < min_seconds:
+        for d in gemm_in:
+            t0 = time.perf_counter()
+            y = oracle.w4a16(d["x"], d["qweight"], d["qzeros"], d["s"], GROUP)
+            t_gemm += time.perf_counter() - t0
+            assert np.isfinite(y).all()
+        t0 = time.perf_counter()
+        oracle.w4a16(gemv_in["x"], gemv_in["qweight"], gemv_in["qzeros"], gemv_in["s"], GROUP)
+        t_gemv += time.perf_counter() - t0
+        reps += 1
+    flops = reps * sum(2.0 * M * N * K for (M, K, N) in GEMM_SHAPES)
     return {"value": round(flops / t_gemm / 1e12, 4), "unit": "TFLOP/s", "cores": int(threads),
-            "kind": "oracle", "seconds": round(t_gemm, 3),
-            "gemv_GBps": round(algo_bytes_w4(K1, N1) / t_gemv / 1e9, 3),
-            "gemv_seconds": round(t_gemv, 4),
-            "sample": "the whole prefill GEMM pair of one step (M=2048; K,N = 4096,14336 and "
-                      "14336,4096) plus one M=1 GEMV, oracle = unpack + fp64 dequant + fp64 BLAS matmul"}
+            "kind": "oracle", "seconds": round(t_gemm + t_gemv, 3), "steps": reps,
+            "gemv_GBps": round(reps * algo_bytes_w4(K1, N1) / t_gemv / 1e9, 3),
+            "sample": "%d whole steps: the prefill GEMM pair (M=2048; K,N = 4096,14336 and "
+                      "14336,4096) and one M=1 GEMV each; oracle = unpack + fp64 dequant + "
+                      "fp64 BLAS matmul; value from the GEMM time" % reps}
+
+
+def calibrate_copy(torch):
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read": COPY_BYTES,
+                      "bytes_written": COPY_BYTES, "launches": 3}), flush=True)
 
 
 def main():
@@ -94,6 +138,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.calibrate_copy:
+        calibrate_copy(torch)
+        return
     tf.load()
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
@@ -180,8 +227,8 @@ def main():
             "peak": PEAK_F16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(tflops / PEAK_F16_TFLOPS, 4),
-            "traffic": None,
-            "kernel": "gemm_kernel<4> (both prefill shapes)",
+            "traffic": recorded_traffic("tf_gemm.hip"),
+            "kernel": "gemm_kernel<4,1> (both prefill shapes)",
         },
         "gemv": {
             "value": round(gemv_gbs, 1),
@@ -190,9 +237,10 @@ def main():
             "bytes_per_launch": gemv_bytes,
             "roofline": {"bound": "hbm", "achieved": round(gemv_gbs, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(gemv_gbs / PEAK_HBM_GBS, 4),
-                         "traffic": None, "kernel": "gemv_kernel<4,1>"},
+                         "traffic": recorded_traffic("tf_gemv.hip"),
+                         "kernel": "gemv_kernel<4,1,16,8,4>"},
         },
-        "gemm_ms": round(gemm_ms, 4),
+        "gemm_ms_per_step": round(gemm_ms, 4),
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline()
