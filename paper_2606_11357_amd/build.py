@@ -32,11 +32,17 @@ FLAGS = [
 ]
 
 
-# Per-source extra flags.  The GEMM keeps its MFMA accumulators in ordinary
-# VGPRs: with the default AGPR form the register allocator rotates the 128
-# loop-carried accumulators through AGPR copies every K step.
+# Per-source extra flags.  The 128-row GEMM keeps its MFMA accumulators in
+# ordinary VGPRs: with the default AGPR form the register allocator rotates the
+# 128 loop-carried accumulators through AGPR copies every K step.  Both GEMMs
+# keep small per-thread arrays (group metadata indexed by the unrolled step)
+# in registers rather than letting the compiler move them to LDS.
+_NO_LDS_PROMOTE = ["-mllvm", "-disable-promote-alloca-to-lds"]
 EXTRA = {
-    "tf_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "tf_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", *_NO_LDS_PROMOTE],
+    # the 256-row GEMM's K step is a fully unrolled 64-slot schedule; let the
+    # unroller expand it however large the kernel around it grows
+    "tf_gemm256.hip": [*_NO_LDS_PROMOTE, "-mllvm", "-pragma-unroll-threshold=1000000"],
 }
 
 

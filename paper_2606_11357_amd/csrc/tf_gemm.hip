@@ -379,11 +379,22 @@ int launch_bits(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t*
 
 }  // namespace
 
-int64_t gemm_workspace_bytes(const Layout&, int64_t) { return 0; }
+// From M = 1024 rows up the 256 x 256 kernel runs when its tiles fill the
+// device or a workspace lets it split K (it is then the only GEMM that uses
+// a workspace); below that its 256-row tiles leave too little parallelism.
+constexpr int64_t kGemm256MinM = 1024;
+static bool use_gemm256(const Layout& L, int64_t M, const void* ws) {
+    return M >= kGemm256MinM && gemm256_supported(L) && (ws != nullptr || gemm256_fills_device(L, M));
+}
+
+int64_t gemm_workspace_bytes(const Layout& L, int64_t M) {
+    return M >= kGemm256MinM ? gemm256_workspace_bytes(L, M) : 0;
+}
 
 int launch_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
-                void*, size_t, hipStream_t s) {
+                void* ws, size_t ws_bytes, hipStream_t s) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
+    if (use_gemm256(L, M, ws)) return launch_gemm256(L, A, pk, C, M, ws, ws_bytes, s);
     return L.bits == 4 ? launch_bits<4>(L, A, pk, C, M, s) : launch_bits<8>(L, A, pk, C, M, s);
 }
 

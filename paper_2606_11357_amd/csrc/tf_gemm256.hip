@@ -1,0 +1,538 @@
+// Prefill GEMM for large M (Section 2.1; Section 4.3 "GEMM microkernel"):
+//   C[M, N] = A[M, K] x dequant(packed)[K, N], fp16 MFMA, fp32 accumulate.
+//
+// One workgroup of four waves per compute unit (one wave per SIMD, so each
+// wave has the whole 512-entry register file: 256 accumulators plus operands).
+// Workgroup tile 256 x 256; each wave owns all 256 rows x 64 columns (one
+// 4-bit panel or two 8-bit panels).  The dequantization of a 32 x 64 weight
+// step (Eq. 2, rounded once) is therefore reused across 16 row blocks: about
+// one vector-ALU instruction per v_mfma_f32_16x16x32_f16, which the SIMD
+// issues while the matrix core works (Sections 4.1.1 and 4.3: dequantize each
+// weight tile once and reuse it for every activation row).
+//  - A (fp16) goes global -> registers -> LDS through three XOR-swizzled
+//    buffers of 256 rows x 32 halves; loads for step s+1 leave at the start of
+//    step s and are written to LDS at its end; one barrier per step.
+//  - The wave's packed atoms are loaded three steps ahead into a register
+//    ring and dequantized one step ahead, straight into the B-operand layout.
+//  - Loads go through buffer resources: the step advances a scalar offset,
+//    and rows past M or panels past N read as zero (hardware range check).
+//  - Tiles are dealt so each XCD (blocks go round-robin over the 8 XCDs)
+//    walks a contiguous band of the tile list; the list runs along whichever
+//    operand is larger so that operand is fetched by fewer XCD caches.
+#include <algorithm>
+
+#include "tf_internal.h"
+
+namespace tf {
+namespace {
+
+constexpr int kBM = 256, kBN = 256, kBK = 32;
+constexpr int kThreads = 256;
+constexpr int kXcds = 8;
+constexpr int kABufs = 4;                // = steps per chunk: buffer index j is static
+constexpr int kCS = 4;                 // steps per 128-row chunk (atom ring size)
+constexpr int kRB = kBM / 16;          // 16-row blocks per wave
+constexpr int kSkMinUnits = 8;         // fewest K chunks per stream-K block
+
+// 16-byte LDS slot of chunk `ch` (0..3) of A row `row` (64-byte rows); the
+// XOR with row bits 2..3 spreads the 16 rows of one ds_read_b128 quarter-wave
+// over distinct bank groups.
+__device__ __forceinline__ int a_slot(int row, int ch) { return row * 4 + (ch ^ ((row >> 2) & 3)); }
+
+// Raw buffer resource over [base, base + bytes): loads past the end return 0.
+// Word 3 = 32-bit data format, no swizzle, for this GPU family.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+// Cache policy of the stream-K partials and counters: sc1, device-coherent
+// (writes reach memory visible to every XCD, reads do not hit a stale line).
+constexpr int kSc1 = 16;
+__device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// acc += a x b on the matrix core with the accumulator pinned to one AGPR
+// quad for the whole loop (source C and destination are the same registers).
+// Written as an asm statement because the register allocator otherwise
+// moves the 256 loop-carried accumulators between AGPRs and VGPRs at every
+// step; the asm is not volatile, so it still schedules freely.
+__device__ __forceinline__ void mfma_acc(float4_t& acc, const half8_t& a, const half8_t& b) {
+    asm("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// The weights go in as the first operand and the activations as the second,
+// so each accumulator block is a 16 (n) x 16 (m) tile of C transposed: lane l
+// holds row m = l % 16 of C and four consecutive columns n = 4 (l / 16) + r,
+// which the epilogue stores as one 8-byte write.
+// The compiler does not see the MFMAs inside the asm statements, so it does
+// not insert the wait states the ISA requires between a matrix instruction
+// writing its accumulator and another instruction reading it (nor between
+// the accumulator initialisation and the first MFMA).  The loop body is its
+// own basic block, so a gap of 32 wait states placed before and after the loop
+// covers both transitions; inside the loop, accumulators are only read by
+// further MFMAs of the same shape (no wait needed) and B operands are produced
+// a whole K step (and a barrier) ahead of their use.
+__device__ __forceinline__ void mfma_hazard_gap() {
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7");
+}
+
+// Workgroup barrier that waits only for this wave's LDS writes, not for the
+// kLead fragment reads issued after them (LDS operations complete in order,
+// so lgkmcnt <= 4 means every earlier one, the writes included, is done):
+// the reads stay in flight across the barrier.  s_waitcnt fields: vmcnt and
+// expcnt at their maximum (no wait), lgkmcnt = 4.
+__device__ __forceinline__ void barrier_after_writes() {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0xC07F | (4 << 8));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// Work split.  Data-parallel (sk.groups == 0): block b computes one whole
+// tile.  Stream-K (sk.groups = G > 0): the tiles x chunks 128-row K chunks of
+// the whole problem, tile-major, are cut into G equal contiguous ranges, one
+// per block; a block walks its range tile by tile, so a tile may be computed
+// in several K segments by consecutive blocks.  Every segment of a split
+// tile parks its fp32 partial tile in the workspace (slot 2v for the first
+// segment of block v's range, 2v + 1 for its last) and counts its arrival on
+// the counter of the tile's first block; the last to arrive adds all
+// partials in K order (so the result does not depend on which block came
+// last), writes C and returns the counter to zero.  Partials and counters are
+// accessed with device-coherent (sc1) loads and stores: the blocks of one
+// tile run on different XCDs, whose L2 caches are not coherent.
+struct StreamK {
+    int groups;               // G, 0 = data-parallel
+    int units;                // tiles * chunks
+    uint32_t* cnt;            // G arrival counters (zero at rest)
+    float* part;              // 2 G partial tiles of kBM x kBN floats
+};
+
+__device__ __forceinline__ int sk_owner(int64_t u, int G, int U) {   // block whose range holds u
+    return (int)(((u + 1) * G - 1) / U);
+}
+__device__ __forceinline__ int sk_begin(int v, int G, int U) { return (int)((int64_t)v * U / G); }
+
+template <int BITS, int MPC>
+__global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
+    const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
+    int M, int K, int N, int gshift, int64_t s_off, int64_t z_off, int na, int ng, int np,
+    int tiles_m, int tiles_n, int col_major, StreamK sk) {
+    constexpr int PW = BITS == 4 ? 64 : 32;
+    constexpr int T = PW / 16;                 // columns per lane per atom
+    constexpr int PANELS = 64 / PW;            // panels per wave
+    constexpr int SPG = kCS / MPC;             // steps per metadata group
+    __shared__ __align__(16) u32x4 As[kABufs][kBM * kBK / 8];
+    __shared__ int last_flag;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int c = lane & 15, kg = lane >> 4;
+    const uint32_t magic = magic_reg();
+    const int steps = na;
+    const int chunks = steps / kCS;            // the launcher requires K % 128 == 0
+    constexpr int kDqSteps = BITS == 4 ? kDqW4Steps : kDqW8Steps;
+
+    uint32_t avoff[4];
+    int aslot[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int idx = tid + kThreads * r;
+        avoff[r] = (uint32_t)(idx >> 2) * (uint32_t)K * 2u + (uint32_t)(idx & 3) * 16u;
+        aslot[r] = a_slot(idx >> 2, idx & 3);
+    }
+    auto store_a = [&](int buf, const u32x4 (&av)[4]) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) As[buf][aslot[r]] = av[r];
+    };
+    auto read_a = [&](int buf, int i) {
+        return __builtin_bit_cast(half8_t, As[buf][a_slot(16 * i + c, kg)]);
+    };
+    struct Meta {
+        uint32_t s[MPC][PANELS][(T + 1) / 2];   // T fp16 scales per group and panel
+        uint32_t z[MPC][PANELS];                // T zero-point bytes
+    };
+    // Group constants per lane column: (s, s), -(1024 + z), -(64 + z).
+    struct Consts {
+        half2_t s2[4];
+        uint32_t nz[4], nz64[4];
+    };
+    auto make_consts = [&](const Meta& mt, int m, Consts& k) {
+#pragma unroll
+        for (int pp = 0; pp < PANELS; ++pp)
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                const uint32_t sh = mt.s[m][pp][t / 2] >> (16 * (t & 1));
+                k.s2[pp * T + t] = as_h2(__builtin_amdgcn_perm(sh, sh, 0x01000100u));
+                const uint32_t n = __builtin_amdgcn_perm(0xE4E4E4E4u, mt.z[m][pp], 0x04000400u | (t * 0x00010001u));
+                k.nz[pp * T + t] = n;
+                k.nz64[pp * T + t] = neg_zero64_pair(n);
+            }
+    };
+    // Dequantization micro-step k of B operand u (0..3) from ring slot `slot`.
+    auto dq_step = [&](int u, int k, const u32x4 (&slot)[PANELS], const Consts& kk, DqState& st) {
+        const int pp = u / T, t = u % T;
+        if constexpr (BITS == 4)
+            dq_w4_step(k, slot[pp][t], magic, kk.nz[u], kk.nz64[u], kk.s2[u], st);
+        else
+            dq_w8_step(k, slot[pp][2 * t], slot[pp][2 * t + 1], kk.nz[u], kk.s2[u], st);
+    };
+    auto dequant = [&](const u32x4 (&slot)[PANELS], const Consts& kk, half8_t (&bop)[4]) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            DqState st;
+#pragma unroll
+            for (int k = 0; k < kDqSteps; ++k) dq_step(u, k, slot, kk, st);
+            bop[u] = __builtin_bit_cast(half8_t, st.out);
+        }
+    };
+
+    // ---- output: 16-row blocks through a per-wave LDS staging area (rows
+    // padded to 144 bytes), leaving as 16-byte stores, eight full 128-byte
+    // rows per store instruction.  get(i, t) yields accumulator block (i, t):
+    // row m = 16 i + c, columns n = 16 t + 4 kg + 0..3 of the wave's tile.
+    // The caller has made sure no wave still reads the A buffers underneath.
+    auto store_tile = [&](int64_t row0, int64_t col0, auto&& get) {
+        uint8_t* stage = reinterpret_cast<uint8_t*>(&As[0][0]) + wave * 4096;
+        constexpr int kStageRow = 144;
+        const bool interior = row0 + kBM <= M && col0 + 64 <= N;
+        const int rr = lane >> 3, cc = lane & 7;      // read-back: row rr (+8), 16-byte chunk cc
+#pragma unroll
+        for (int i = 0; i < kRB; ++i) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const float4_t a = get(i, t);
+                const half2_t lo = {(_Float16)a[0], (_Float16)a[1]};
+                const half2_t hi = {(_Float16)a[2], (_Float16)a[3]};
+                *reinterpret_cast<uint2*>(stage + c * kStageRow + 32 * t + 8 * kg) = uint2{as_u32(lo), as_u32(hi)};
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);       // lgkmcnt(0): this wave's stores landed
+            u32x4 v[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+                v[h] = *reinterpret_cast<const u32x4*>(stage + (rr + 8 * h) * kStageRow + 16 * cc);
+            __builtin_amdgcn_s_waitcnt(0xC07F);       // reads done before the area is rewritten
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int64_t m = row0 + 16 * i + rr + 8 * h, n = col0 + 8 * cc;   // N % 8 == 0
+                if (interior || (m < M && n < N)) *reinterpret_cast<u32x4*>(C + m * N + n) = v[h];
+            }
+        }
+    };
+
+    float4_t acc[kRB][4];
+
+    // ---- one K segment: chunks [c0, c1) of tile `tile` into acc.
+    auto segment = [&](int tile, int c0, int c1, int64_t& row0_out, int64_t& col0_out) {
+        __syncthreads();   // the previous segment's output staging is done with the LDS
+        // (uniform values; readfirstlane keeps the buffer resources in scalars)
+        const int tm = __builtin_amdgcn_readfirstlane(col_major ? tile % tiles_m : tile / tiles_n);
+        const int tn = __builtin_amdgcn_readfirstlane(col_major ? tile / tiles_m : tile % tiles_n);
+        const int64_t row0 = (int64_t)tm * kBM;
+        const int64_t col0 = (int64_t)tn * kBN + wave * 64;      // this wave's 64 columns
+        row0_out = row0;
+        col0_out = col0;
+
+        // A: the tile's rows as one buffer (rows past M read as zero); 256 rows
+        // x 32 halves per step = 1024 16-byte chunks, 4 per thread.
+        const int rows = (int)min<int64_t>(kBM, (int64_t)M - row0);
+        const __amdgpu_buffer_rsrc_t a_rsrc = make_rsrc(A + row0 * K, (uint32_t)rows * (uint32_t)K * 2u);
+        auto load_a = [&](int step, u32x4 (&av)[4]) {
+            const uint32_t soff = (uint32_t)min(step, steps - 1) * (kBK * 2);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) av[r] = load16(a_rsrc, avoff[r], soff);
+        };
+        // B: packed panels and metadata as buffers; a panel past N is an
+        // empty buffer (reads zero; its columns are never stored).
+        __amdgpu_buffer_rsrc_t wr[PANELS], sr[PANELS], zr[PANELS];
+#pragma unroll
+        for (int pp = 0; pp < PANELS; ++pp) {
+            const int64_t panel = col0 / PW + pp;
+            const bool in = panel < np;
+            const int64_t pc = in ? panel : 0;
+            wr[pp] = make_rsrc(packed + pc * na * kAtomBytes, in ? (uint32_t)na * kAtomBytes : 0u);
+            sr[pp] = make_rsrc(packed + s_off + pc * ng * PW * 2, in ? (uint32_t)(ng * PW * 2) : 0u);
+            zr[pp] = make_rsrc(packed + z_off + pc * ng * PW, in ? (uint32_t)(ng * PW) : 0u);
+        }
+        u32x4 ring[kCS][PANELS];
+        auto load_atom = [&](int step, u32x4 (&slot)[PANELS]) {
+            const uint32_t soff = (uint32_t)min(step, steps - 1) * kAtomBytes;
+#pragma unroll
+            for (int pp = 0; pp < PANELS; ++pp) slot[pp] = load16(wr[pp], (uint32_t)lane * 16u, soff);
+        };
+        auto load_meta = [&](int ch, Meta& mt) {
+            ch = min(ch, chunks - 1);
+#pragma unroll
+            for (int m = 0; m < MPC; ++m) {
+                const uint32_t g = (uint32_t)((ch * kCS + m * SPG) * kAtomK) >> gshift;
+#pragma unroll
+                for (int pp = 0; pp < PANELS; ++pp) {
+                    if constexpr (BITS == 4) {
+                        const uint2 sv = __builtin_bit_cast(
+                            uint2, __builtin_amdgcn_raw_buffer_load_b64(sr[pp], (uint32_t)c * 8u, g * (PW * 2), 0));
+                        mt.s[m][pp][0] = sv.x;
+                        mt.s[m][pp][1] = sv.y;
+                        mt.z[m][pp] = __builtin_amdgcn_raw_buffer_load_b32(zr[pp], (uint32_t)c * 4u, g * PW, 0);
+                    } else {
+                        mt.s[m][pp][0] =
+                            __builtin_amdgcn_raw_buffer_load_b32(sr[pp], (uint32_t)c * 4u, g * (PW * 2), 0);
+                        mt.z[m][pp] = __builtin_amdgcn_raw_buffer_load_b16(zr[pp], (uint32_t)c * 2u, g * PW, 0);
+                    }
+                }
+            }
+        };
+
+#pragma unroll
+        for (int i = 0; i < kRB; ++i)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) acc[i][t] = float4_t{0.f, 0.f, 0.f, 0.f};
+
+        // Prologue (s0 = first step): A of steps s0, s0+1 in LDS, A of s0+2,
+        // s0+3 in flight; atoms of steps s0..s0+3 and metadata of the first
+        // two chunks requested; B operands of step s0; the first A fragments
+        // of step s0 read.  A register set j holds the A of a step = j mod 4.
+        const int s0 = c0 * kCS;
+        u32x4 ra[kCS][4];
+        load_a(s0, ra[0]);
+        store_a(0, ra[0]);
+        load_a(s0 + 1, ra[1]);
+        store_a(1, ra[1]);
+        load_a(s0 + 2, ra[2]);
+        load_a(s0 + 3, ra[3]);
+#pragma unroll
+        for (int j = 0; j < kCS; ++j) load_atom(s0 + j, ring[j]);
+        Meta mcur, mnext;
+        load_meta(c0, mcur);
+        load_meta(c0 + 1, mnext);
+        Consts kc;
+        make_consts(mcur, 0, kc);
+        half8_t bop[4];
+        dequant(ring[0], kc, bop);
+        __syncthreads();
+        // A fragment ring: block i of every step uses entry i % 8 (16 blocks
+        // per step, so the pattern repeats exactly from step to step); reads
+        // run four blocks ahead.
+        constexpr int kLead = 4, kRing = 8;
+        half8_t af[kRing];
+#pragma unroll
+        for (int i = 0; i < kLead; ++i) af[i] = read_a(0, i);
+        mfma_hazard_gap();
+
+        // One K step s (j = s mod 4), as 64 MFMA slots (row block i = slot / 4,
+        // column block t = slot % 4), each followed by at most one other
+        // instruction group, fixed by scheduling fences:
+        //   slot 0        loads of A for step s+4 (into register set j, free
+        //                 since A of step s went to LDS during step s-2) and of
+        //                 the atoms for step s+4 (into the ring slot of step s,
+        //                 whose operands were formed during step s-1)
+        //   slots 4i      A fragment of row block i + 4 from LDS (eight-entry
+        //                 ring, so each LDS read has four blocks to land); for
+        //                 i = 12..15 fragment i - 12 of step s+1 instead
+        //                 (written before the previous barrier)
+        //   slots 4..55   the 52 (4-bit) or 48 (8-bit) dequantization
+        //                 micro-steps of step s+1's B operands, one vector
+        //                 instruction each, issued while the matrix core works
+        //   slots 40..43  A of step s+2 written to LDS (buffer last read in step
+        //                 s-2, before an earlier barrier); these writes come
+        //                 before the reads for step s+1, so the barrier's wait
+        //                 for "all but the last four LDS operations" covers them
+        // then one barrier, which waits for this wave's LDS writes only.
+        for (int ch = c0; ch < c1; ++ch) {
+#pragma unroll
+            for (int j = 0; j < kCS; ++j) {
+                const int step = ch * kCS + j;
+                const int buf = j;                        // step % kABufs (s0 % 4 == 0)
+                if (j == kCS - 1) {
+                    mcur = mnext;                         // first group of the next chunk
+                    load_meta(ch + 2, mnext);
+                    make_consts(mcur, 0, kc);
+                } else if ((j + 1) % SPG == 0) {
+                    make_consts(mcur, (j + 1) / SPG, kc); // next step starts a new group
+                }
+                half8_t bnext[4];
+                DqState st[4];
+#pragma unroll
+                for (int q = 0; q < 4 * kRB; ++q) {
+                    const int i = q / 4, t = q % 4;
+                    __builtin_amdgcn_sched_barrier(0);
+                    mfma_acc(acc[i][t], bop[t], af[i % kRing]);
+                    if (q == 0) {
+                        load_a(step + 4, ra[j]);
+                        load_atom(step + 4, ring[j]);
+                    }
+                    if (t == 0 && i + kLead < kRB) af[(i + kLead) % kRing] = read_a(buf, i + kLead);
+                    if (t == 0 && i + kLead >= kRB)
+                        af[i + kLead - kRB] = read_a((j + 1) % kABufs, i + kLead - kRB);
+                    if (q >= 4 && q < 4 + 4 * kDqSteps) {
+                        const int o = q - 4, u = o / kDqSteps, k = o % kDqSteps;
+                        dq_step(u, k, ring[(j + 1) % kCS], kc, st[u]);
+                        if (k == kDqSteps - 1) bnext[u] = __builtin_bit_cast(half8_t, st[u].out);
+                    }
+                    if (q >= 40 && q < 44) {
+                        const int r = q - 40;
+                        As[(j + 2) % kABufs][aslot[r]] = ra[(j + 2) % kCS][r];
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int t = 0; t < 4; ++t) bop[t] = bnext[t];
+                barrier_after_writes();
+            }
+        }
+        mfma_hazard_gap();
+        __syncthreads();   // every wave done with the A buffers (the output staging reuses them)
+    };
+
+    // Range of 128-row K chunks ("units", tile-major) this block computes.
+    const int G = sk.groups, U = sk.units, b = blockIdx.x;
+    int v = 0, ua, ub;
+    if (G == 0) {
+        // Data-parallel: XCD band of the tile list; block b runs on XCD b % 8
+        // and takes the (b / 8)-th tile of that XCD's contiguous band.
+        const int total = tiles_m * tiles_n;
+        const int per = total / kXcds, rem = total % kXcds;
+        const int x = b % kXcds, i = b / kXcds;
+        ua = (x * per + min(x, rem) + i) * chunks;
+        ub = ua + chunks;
+    } else {
+        // Stream-K: virtual block index v numbers the blocks XCD by XCD, so
+        // each XCD walks a contiguous part of the unit list.
+        v = (G % kXcds == 0) ? (b % kXcds) * (G / kXcds) + b / kXcds : b;
+        ua = sk_begin(v, G, U);
+        ub = sk_begin(v + 1, G, U);
+    }
+    auto whole = [&](int i, int t) { return acc[i][t]; };
+    int64_t row0, col0;
+    for (int u = ua; u < ub;) {
+        const int tile = u / chunks, c0 = u % chunks;
+        const int c1 = min(chunks, c0 + (ub - u));
+        segment(tile, c0, c1, row0, col0);
+        if (c0 == 0 && c1 == chunks) {
+            store_tile(row0, col0, whole);
+        } else {
+            // Park the partial: wave w's 256 x 64 part at w * 16384 floats,
+            // block (i, t) as 64 consecutive float4 (one per lane).
+            const int slot = 2 * v + (u == ua ? 0 : 1);
+            float* part = sk.part + (int64_t)slot * (kBM * kBN);
+            const __amdgpu_buffer_rsrc_t pr = make_rsrc(part + wave * (kBM * 64), kBM * 64 * 4);
+#pragma unroll
+            for (int i = 0; i < kRB; ++i)
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, acc[i][t]), pr,
+                                                           (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, kSc1);
+            __builtin_amdgcn_s_waitcnt(0);                // this thread's partial stores have completed
+            __syncthreads();
+            const int t0 = tile * chunks;
+            const int vlo = sk_owner(t0, G, U), vhi = sk_owner(t0 + chunks - 1, G, U);
+            if (tid == 0)
+                last_flag = __hip_atomic_fetch_add(&sk.cnt[vlo], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                            (uint32_t)(vhi - vlo);
+            __syncthreads();
+            if (last_flag) {
+                // Sum the segments in K order (block vlo first): the partials
+                // of the blocks before this one, this block's own from its
+                // registers, then those after it.
+                auto partial_of = [&](int w, int i, int t) {
+                    const int sw = 2 * w + (sk_begin(w, G, U) >= t0 ? 0 : 1);
+                    const __amdgpu_buffer_rsrc_t q =
+                        make_rsrc(sk.part + (int64_t)sw * (kBM * kBN) + wave * (kBM * 64), kBM * 64 * 4);
+                    return __builtin_bit_cast(float4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                            q, (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, kSc1));
+                };
+                auto total_of = [&](int i, int t) {
+                    float4_t r = {0.f, 0.f, 0.f, 0.f};
+                    for (int w = vlo; w < v; ++w) r += partial_of(w, i, t);
+                    r += acc[i][t];
+                    for (int w = v + 1; w <= vhi; ++w) r += partial_of(w, i, t);
+                    return r;
+                };
+                store_tile(row0, col0, total_of);
+                if (tid == 0) __hip_atomic_store(&sk.cnt[vlo], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        u += c1 - c0;
+    }
+}
+
+template <int BITS, int MPC>
+int launch_mpc(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
+               StreamK sk, int tiles_m, int tiles_n, hipStream_t s) {
+    const int gshift = __builtin_ctz((unsigned)L.group);
+    // Walk the tile list along N (column-major) when the weights outweigh the
+    // activations: each XCD band then covers fewer weight panels.
+    const int64_t a_bytes = M * L.K * 2, w_bytes = L.total;
+    const int col_major = w_bytes > a_bytes ? 1 : 0;
+    const unsigned grid = sk.groups ? (unsigned)sk.groups : (unsigned)(tiles_m * tiles_n);
+    return launch(gemm256_kernel<BITS, MPC>, dim3(grid), dim3(kThreads), 0, s, A, pk, C, (int)M,
+                  (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na, (int)L.ng, (int)L.np,
+                  tiles_m, tiles_n, col_major, sk);
+}
+
+// Compute units of the current device (cached per device; the value never
+// changes, so a race between first callers only stores the same number).
+int device_cus() {
+    static int cus[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return kSkMaxGroups;
+    if (cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            return kSkMaxGroups;
+        cus[dev] = n;
+    }
+    return cus[dev];
+}
+
+}  // namespace
+
+bool gemm256_supported(const Layout& L) {
+    return L.K % (kBK * kCS) == 0 && (L.group & (L.group - 1)) == 0;
+}
+
+// Stream-K is planned when the 256 x 256 tiles do not fill whole waves of
+// kSkMaxGroups blocks; its workspace is the arrival counters (at the shared
+// counter offset 0) and two partial tiles per block.
+int64_t gemm256_workspace_bytes(const Layout& L, int64_t M) {
+    const int64_t tiles = ((M + kBM - 1) / kBM) * ((L.N + kBN - 1) / kBN);
+    if (!gemm256_supported(L) || tiles % kSkMaxGroups == 0) return 0;
+    return kWsCounterBytes + (int64_t)2 * kSkMaxGroups * kBM * kBN * 4;
+}
+
+int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
+                   void* ws, size_t ws_bytes, hipStream_t s) {
+    const int tiles_m = (int)((M + kBM - 1) / kBM);
+    const int tiles_n = (int)((L.N + kBN - 1) / kBN);
+    const int tiles = tiles_m * tiles_n, chunks = (int)(L.K / (kBK * kCS));
+    const int64_t need = gemm256_workspace_bytes(L, M);
+    const int cus = device_cus();
+    StreamK sk{0, 0, nullptr, nullptr};
+    // Whole tiles while they keep at least 80% of the launch's block slots busy
+    // (ceil(tiles / cus) waves of cus blocks), stream-K below that, with at
+    // least kSkMinUnits K chunks per block.
+    const int64_t waves = (tiles + cus - 1) / cus;
+    const bool dp_ok = 5 * (int64_t)tiles >= 4 * waves * cus;
+    if (ws && need > 0 && (int64_t)ws_bytes >= need && !dp_ok) {
+        const int64_t units = (int64_t)tiles * chunks;
+        int G = (int)std::min<int64_t>(std::min(cus, kSkMaxGroups), std::max<int64_t>(1, units / kSkMinUnits));
+        if (G > kXcds) G -= G % kXcds;
+        sk = StreamK{G, (int)units, static_cast<uint32_t*>(ws),
+                     reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes)};
+    }
+    const int chunk_rows = kBK * kCS;
+    const int mpc = L.group >= chunk_rows ? 1 : chunk_rows / L.group;
+    if (L.bits == 4) {
+        if (mpc == 1) return launch_mpc<4, 1>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+        if (mpc == 2) return launch_mpc<4, 2>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+        return launch_mpc<4, 4>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+    }
+    if (mpc == 1) return launch_mpc<8, 1>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+    if (mpc == 2) return launch_mpc<8, 2>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+    return launch_mpc<8, 4>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+}
+
+bool gemm256_fills_device(const Layout& L, int64_t M) {
+    const int64_t tiles = ((M + kBM - 1) / kBM) * ((L.N + kBN - 1) / kBN);
+    return 4 * tiles >= 3 * (int64_t)device_cus();
+}
+
+}  // namespace tf

@@ -378,7 +378,6 @@ inline GemvPlan plan_gemv(const Layout& L, int64_t M) {
 // the largest panel count any shape can have, so every call finds its
 // counters where an earlier call (of any shape) left them at zero; then the
 // per-slice partial sums, which are always written before they are read.
-constexpr int64_t kCounterBytes = (TF_MAX_DIM / 32) * 4;
 
 
 template <int BITS, int M, int APG>
@@ -388,7 +387,7 @@ int launch_g(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C,
     const GemvPlan sp = plan_gemv(L, M);
     const bool split = ws != nullptr && sp.S > 1;
     uint32_t* cnt = split ? static_cast<uint32_t*>(ws) : nullptr;
-    float* part = split ? reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kCounterBytes) : nullptr;
+    float* part = split ? reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes) : nullptr;
     const int S = split ? sp.S : 1;
     const int AS = split ? sp.AS : (int)L.na;
     return launch(gemv_kernel<BITS, M, WAVES, kGemvU, APG>, dim3((unsigned)L.np, (unsigned)S),
@@ -427,7 +426,7 @@ int64_t gemv_workspace_bytes(const Layout& L, int64_t M) {
     if (M < 1 || M > TF_GEMV_MAX_M) return 0;
     const GemvPlan sp = plan_gemv(L, M);
     if (sp.S <= 1) return 0;
-    return kCounterBytes + align256((int64_t)L.np * sp.S * M * L.pw * 4);
+    return kWsCounterBytes + align256((int64_t)L.np * sp.S * M * L.pw * 4);
 }
 
 int launch_gemv(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,

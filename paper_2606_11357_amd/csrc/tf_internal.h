@@ -41,6 +41,13 @@ namespace tf {
 // Columns past N (last panel) hold q = z = 0 and s = 0, i.e. weight 0.
 // ---------------------------------------------------------------------------
 constexpr int kLayoutVersion = 1;
+
+// Workspace of the matmul entry points: arrival counters first, in a region
+// of fixed size at offset 0 (every call leaves the counters it used at zero,
+// so one zero-filled buffer serves calls of any shape), then partial sums.
+constexpr int64_t kWsCounterBytes = (TF_MAX_DIM / 32) * 4;
+// Most workgroups a stream-K GEMM launch uses (sizes its workspace).
+constexpr int kSkMaxGroups = 256;
 constexpr int kAtomK = 32;
 constexpr int kAtomBytes = 1024;
 
@@ -119,35 +126,48 @@ __device__ __forceinline__ uint32_t magic_reg() {
     return m;
 }
 
-// Unpack (Section 4.3): one packed 4-bit dword -> four half2 K-pairs holding
-// (1024 + q[k], 1024 + q[k+1]) for row offsets (0,1), (2,3), (4,5), (6,7).
-// `magic` = kMagic2 (pass magic_reg()).
-__device__ __forceinline__ void w4_code_pairs(uint32_t w, uint32_t magic, uint32_t out[4]) {
-    out[0] = (w & 0x000F000Fu) | magic;
-    out[1] = ((w >> 4) & 0x000F000Fu) | magic;
-    out[2] = ((w >> 8) & 0x000F000Fu) | magic;
-    out[3] = ((w >> 12) & 0x000F000Fu) | magic;
+// Unpack primitives (Section 4.3).  `magic` = kMagic2 (pass magic_reg()).
+// Low nibbles of both halves: (1024 + q, 1024 + q') for the nibbles in bits
+// 0..3 and 16..19 of x.
+__device__ __forceinline__ uint32_t w4_pair_lo(uint32_t x, uint32_t magic) {
+    return (x & 0x000F000Fu) | magic;
+}
+// Nibbles in bits 4..7 and 20..23 of x, read without a shift:
+// (1024 + 16 q, 1024 + 16 q'), still exact fp16 integers.
+__device__ __forceinline__ uint32_t w4_pair_hi_x16(uint32_t x, uint32_t magic) {
+    return (x & 0x00F000F0u) | magic;
+}
+// Bytes b, b+1 of an 8-bit dword as (1024 + q, 1024 + q'): v_perm_b32 picks
+// bytes of the second operand with selector values 0-3 and of the first
+// (0x64 bytes) with 4; `hi` selects bytes 2, 3 instead of 0, 1.
+__device__ __forceinline__ uint32_t w8_pair(uint32_t w, bool hi) {
+    return __builtin_amdgcn_perm(0x64646464u, w, hi ? 0x04030402u : 0x04010400u);
 }
 
-// Cheaper variant for sums: the odd pairs are read without a shift, as
-// (1024 + 16 q[k], 1024 + 16 q[k+1]) (nibble in bits 4..7 of each half, still
-// an exact fp16 integer).  out[0], out[2]: rows (0,1), (4,5) as 1024 + q;
-// out[1], out[3]: rows (2,3), (6,7) as 1024 + 16 q.  `magic` = kMagic2.
+// One packed 4-bit dword -> four half2 K-pairs (1024 + q[k], 1024 + q[k+1])
+// for row offsets (0,1), (2,3), (4,5), (6,7).
+__device__ __forceinline__ void w4_code_pairs(uint32_t w, uint32_t magic, uint32_t out[4]) {
+    out[0] = w4_pair_lo(w, magic);
+    out[1] = w4_pair_lo(w >> 4, magic);
+    out[2] = w4_pair_lo(w >> 8, magic);
+    out[3] = w4_pair_lo(w >> 12, magic);
+}
+
+// Cheaper variant for sums: out[0], out[2] are rows (0,1), (4,5) as 1024 + q;
+// out[1], out[3] are rows (2,3), (6,7) as 1024 + 16 q.
 __device__ __forceinline__ void w4_code_pairs_x16(uint32_t w, uint32_t magic, uint32_t out[4]) {
     const uint32_t w8 = w >> 8;
-    out[0] = (w & 0x000F000Fu) | magic;
-    out[1] = (w & 0x00F000F0u) | magic;
-    out[2] = (w8 & 0x000F000Fu) | magic;
-    out[3] = (w8 & 0x00F000F0u) | magic;
+    out[0] = w4_pair_lo(w, magic);
+    out[1] = w4_pair_hi_x16(w, magic);
+    out[2] = w4_pair_lo(w8, magic);
+    out[3] = w4_pair_hi_x16(w8, magic);
 }
 
-// Unpack one 8-bit dword (rows r..r+3, lowest byte first) -> two half2 pairs
+// One 8-bit dword (rows r..r+3, lowest byte first) -> two half2 pairs
 // (1024 + q[r], 1024 + q[r+1]) and (1024 + q[r+2], 1024 + q[r+3]).
-// v_perm_b32 selector bytes 0-3 pick bytes of the second operand, 4-7 bytes
-// of the first; 0x64 comes from the constant.
 __device__ __forceinline__ void w8_code_pairs(uint32_t w, uint32_t out[2]) {
-    out[0] = __builtin_amdgcn_perm(0x64646464u, w, 0x04010400u);
-    out[1] = __builtin_amdgcn_perm(0x64646464u, w, 0x04030402u);
+    out[0] = w8_pair(w, false);
+    out[1] = w8_pair(w, true);
 }
 
 // -(1024 + z) as an fp16 pair, exact for 0 <= z <= 255.
@@ -156,50 +176,86 @@ __device__ __forceinline__ uint32_t neg_zero_pair(uint32_t z) {
     return h | (h << 16);
 }
 
-// Eq. 2 on a code pair, rounded once: (1024+q) - (1024+z) = q - z exactly in
-// fp16 (|q - z| <= 255), then one fp16 multiply by s: RNE(s * (q - z)).
-__device__ __forceinline__ half2_t dq_pair(uint32_t codes, uint32_t negz2, half2_t s2) {
-#pragma clang fp contract(off)
-    half2_t d = as_h2(codes) + as_h2(negz2);
-    return d * s2;
-}
-
 // -(64 + z) as an fp16 pair from neg_zero_pair(z): -(1024 + z) + 960, exact.
 __device__ __forceinline__ uint32_t neg_zero64_pair(uint32_t negz2) {
     const half2_t c960 = {(_Float16)960.0f, (_Float16)960.0f};
     return as_u32(as_h2(negz2) + c960);
 }
 
-// Eight dequantized fp16 weights (one MFMA B operand) from one 4-bit dword,
-// each RNE(s * (q - z)) rounded once (Eq. 2).  Rows (0,1) and (4,5) are read
-// as 1024 + q and reduced by (1024 + z); rows (2,3) and (6,7) are read without
-// a shift as 1024 + 16 q and reduced by one fused multiply-add,
-// (1024 + 16 q) / 16 - (64 + z), whose exact value q - z is an fp16 integer,
-// so the single rounding of the fma is exact.  Then one multiply by s.
+// Dequantization of eight weights (one MFMA B operand) as a fixed sequence of
+// single vector instructions ("micro-steps"), so that a kernel can place them
+// one by one between matrix instructions.  dq_w4_dword / dq_w8_dwords run
+// the whole sequence; every kernel and tf_dequant use this code.
+//
+// 4-bit, 13 steps:
+//   0      w8 = w >> 8
+//   1..4   unpack: rows (0,1), (4,5) as 1024 + q; rows (2,3), (6,7) read without
+//          a shift as 1024 + 16 q (see w4_code_pairs_x16)
+//   5, 6   (1024 + q) - (1024 + z) = q - z, exact
+//   7, 8   (1024 + 16 q) / 16 - (64 + z) by one fused multiply-add: its exact
+//          value q - z is an fp16 integer, so its single rounding is exact
+//   9..12  one fp16 multiply by s: RNE(s * (q - z)) (Eq. 2), rounded once
 // negz2 = neg_zero_pair(z), negz64 = neg_zero64_pair(negz2), s2 = (s, s).
+struct DqState {
+    uint32_t w8;
+    uint32_t p[4];   // four half2 K-pairs
+    u32x4 out;       // the finished operand, pair j in dword j
+};
+constexpr int kDqW4Steps = 13, kDqW8Steps = 12;
+
+__device__ __forceinline__ void dq_w4_step(int k, uint32_t w, uint32_t magic, uint32_t negz2,
+                                           uint32_t negz64, half2_t s2, DqState& st) {
+#pragma clang fp contract(off)
+    const half2_t sixteenth = {(_Float16)0.0625f, (_Float16)0.0625f};
+    switch (k) {
+        case 0: st.w8 = w >> 8; break;
+        case 1: st.p[0] = w4_pair_lo(w, magic); break;
+        case 2: st.p[1] = w4_pair_hi_x16(w, magic); break;
+        case 3: st.p[2] = w4_pair_lo(st.w8, magic); break;
+        case 4: st.p[3] = w4_pair_hi_x16(st.w8, magic); break;
+        case 5: st.p[0] = as_u32(as_h2(st.p[0]) + as_h2(negz2)); break;
+        case 6: st.p[2] = as_u32(as_h2(st.p[2]) + as_h2(negz2)); break;
+        case 7: st.p[1] = as_u32(__builtin_elementwise_fma(as_h2(st.p[1]), sixteenth, as_h2(negz64))); break;
+        case 8: st.p[3] = as_u32(__builtin_elementwise_fma(as_h2(st.p[3]), sixteenth, as_h2(negz64))); break;
+        default: st.out[k - 9] = as_u32(as_h2(st.p[k - 9]) * s2); break;
+    }
+}
+
+// 8-bit, 12 steps on two dwords (rows 0..3, 4..7):
+//   0..3   unpack to four pairs 1024 + q (see w8_code_pairs)
+//   4..7   (1024 + q) - (1024 + z) = q - z, exact (|q - z| <= 255)
+//   8..11  one fp16 multiply by s (Eq. 2), rounded once
+__device__ __forceinline__ void dq_w8_step(int k, uint32_t w0, uint32_t w1, uint32_t negz2,
+                                           half2_t s2, DqState& st) {
+#pragma clang fp contract(off)
+    switch (k) {
+        case 0: st.p[0] = w8_pair(w0, false); break;
+        case 1: st.p[1] = w8_pair(w0, true); break;
+        case 2: st.p[2] = w8_pair(w1, false); break;
+        case 3: st.p[3] = w8_pair(w1, true); break;
+        case 4: case 5: case 6: case 7:
+            st.p[k - 4] = as_u32(as_h2(st.p[k - 4]) + as_h2(negz2));
+            break;
+        default: st.out[k - 8] = as_u32(as_h2(st.p[k - 8]) * s2); break;
+    }
+}
+
+// Eight dequantized fp16 weights from one 4-bit dword, each RNE(s * (q - z)).
 __device__ __forceinline__ half8_t dq_w4_dword(uint32_t w, uint32_t magic, uint32_t negz2,
                                                uint32_t negz64, half2_t s2) {
-#pragma clang fp contract(off)
-    uint32_t c[4];
-    w4_code_pairs_x16(w, magic, c);
-    const half2_t sixteenth = {(_Float16)0.0625f, (_Float16)0.0625f};
-    const half2_t d0 = as_h2(c[0]) + as_h2(negz2);
-    const half2_t d2 = as_h2(c[2]) + as_h2(negz2);
-    const half2_t d1 = __builtin_elementwise_fma(as_h2(c[1]), sixteenth, as_h2(negz64));
-    const half2_t d3 = __builtin_elementwise_fma(as_h2(c[3]), sixteenth, as_h2(negz64));
-    const half2_t p0 = d0 * s2, p1 = d1 * s2, p2 = d2 * s2, p3 = d3 * s2;
-    return half8_t{p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};
+    DqState st;
+#pragma unroll
+    for (int k = 0; k < kDqW4Steps; ++k) dq_w4_step(k, w, magic, negz2, negz64, s2, st);
+    return __builtin_bit_cast(half8_t, st.out);
 }
 
 // Eight dequantized fp16 weights from two 8-bit dwords (rows 0..3, 4..7).
 __device__ __forceinline__ half8_t dq_w8_dwords(uint32_t w0, uint32_t w1, uint32_t negz2,
                                                 half2_t s2) {
-    uint32_t c0[2], c1[2];
-    w8_code_pairs(w0, c0);
-    w8_code_pairs(w1, c1);
-    half2_t p0 = dq_pair(c0[0], negz2, s2), p1 = dq_pair(c0[1], negz2, s2);
-    half2_t p2 = dq_pair(c1[0], negz2, s2), p3 = dq_pair(c1[1], negz2, s2);
-    return half8_t{p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};
+    DqState st;
+#pragma unroll
+    for (int k = 0; k < kDqW8Steps; ++k) dq_w8_step(k, w0, w1, negz2, s2, st);
+    return __builtin_bit_cast(half8_t, st.out);
 }
 
 }  // namespace tf
@@ -219,6 +275,11 @@ int64_t gemv_workspace_bytes(const Layout& L, int64_t M);
 int launch_gemv(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, hipStream_t s);
 int64_t gemm_workspace_bytes(const Layout& L, int64_t M);
+bool gemm256_supported(const Layout& L);
+bool gemm256_fills_device(const Layout& L, int64_t M);
+int64_t gemm256_workspace_bytes(const Layout& L, int64_t M);
+int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
+                   void* ws, size_t ws_bytes, hipStream_t s);
 int launch_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, size_t ws_bytes, hipStream_t s);
 }  // namespace tf

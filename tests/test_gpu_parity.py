@@ -158,7 +158,10 @@ GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 2
                (8, 33, 256, 40, 128), (8, 130, 384, 104, 128), (4, 9, 96, 8, 32),
                (4, 300, 1024, 520, 128), (8, 64, 128, 4096, 128), (4, 1, 256, 64, 128),
                (4, 200, 512, 328, 32), (8, 150, 512, 264, 64), (8, 140, 384, 72, 32),
-               (4, 257, 768, 1000, 256), (8, 129, 1024, 200, 1024), (4, 96, 1152, 392, 96)]
+               (4, 257, 768, 1000, 256), (8, 129, 1024, 200, 1024), (4, 96, 1152, 392, 96),
+               (4, 600, 1024, 1040, 128), (8, 520, 512, 776, 64), (4, 513, 256, 2056, 32),
+               (4, 1100, 512, 1040, 128), (8, 1030, 512, 776, 64), (4, 1280, 256, 520, 32),
+               (8, 1025, 1024, 264, 1024), (4, 1024, 640, 2048, 64)]
 
 
 @pytest.mark.parametrize("bits,M,K,N,G", GEMM_SHAPES)
@@ -169,7 +172,8 @@ def test_gemm_parity_small(tf, bits, M, K, N, G):
 
 @pytest.mark.parametrize("kind,bits,M,K,N", [("gemv", 4, 8, 4096, 1024), ("gemv", 8, 8, 4096, 512),
                                              ("gemm", 8, 256, 4096, 512), ("gemm", 4, 200, 8192, 256),
-                                             ("gemv", 4, 1, 32768, 64)])
+                                             ("gemv", 4, 1, 32768, 64), ("gemm", 4, 1030, 8192, 512),
+                                             ("gemm", 8, 1024, 4096, 768)])
 def test_integer_invariant_bitexact(tf, kind, bits, M, K, N):
     """s = 1, z = 0, integer x in [-3, 3]: every partial sum is an integer below
     2^24, so the fp16 output must be RNE of the exact integer matmul."""
@@ -242,7 +246,38 @@ def test_workspace_shared_across_shapes(tf):
                       f"shared workspace, case {i}: W{bits} {M}x{K}x{N}")
 
 
-@pytest.mark.parametrize("kind,M", [("gemv", 1), ("gemv", 8), ("gemm", 300)])
+@pytest.mark.parametrize("bits,M,K,N,G", [(4, 1300, 2048, 1000, 128), (8, 1520, 1024, 776, 64),
+                                           (4, 2048, 1024, 4096, 32), (4, 1100, 3072, 2320, 128)])
+def test_gemm_workspace_modes(tf, bits, M, K, N, G):
+    """The stream-K split (workspace) and the whole-tile kernels (no workspace)
+    both meet the bar; a stream-K result is bitwise repeatable and its
+    workspace serves the next call at once."""
+    d = make_inputs(bits, M, K, N, group=G, seed=M + N)
+    packed = pack(tf, d)
+    want = ref(d)
+    need = tf.workspace_bytes(bits, M, K, N, G)
+    ws = torch.zeros(need + 256, dtype=torch.uint8, device="cuda") if need else False
+    a = run(tf, "gemm", d, packed, workspace=ws)
+    b = run(tf, "gemm", d, packed, workspace=ws)
+    np.testing.assert_array_equal(a.view(np.uint16), b.view(np.uint16))
+    c = run(tf, "gemm", d, packed, workspace=False)
+    assert_parity(a, want, f"gemm W{bits} {M}x{K}x{N} with workspace")
+    assert_parity(c, want, f"gemm W{bits} {M}x{K}x{N} without workspace")
+
+
+def test_workspace_shared_gemm_gemv(tf):
+    """One workspace serves split-K GEMVs and stream-K GEMMs in turn."""
+    cases = [("gemm", 4, 1300, 1024, 1000), ("gemv", 4, 1, 14336, 4096), ("gemm", 8, 1600, 2048, 520),
+             ("gemv", 8, 3, 8192, 520), ("gemm", 4, 1300, 1024, 1000)]
+    need = max(tf.workspace_bytes(b, m, k, n) for _, b, m, k, n in cases)
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    for i, (kind, bits, M, K, N) in enumerate(cases):
+        d = make_inputs(bits, M, K, N, seed=200 + i)
+        assert_parity(run(tf, kind, d, pack(tf, d), workspace=ws), ref(d),
+                      f"shared workspace, case {i}: {kind} W{bits} {M}x{K}x{N}")
+
+
+@pytest.mark.parametrize("kind,M", [("gemv", 1), ("gemv", 8), ("gemm", 300), ("gemm", 1300)])
 def test_bitwise_reproducible(tf, kind, M):
     d = make_inputs(4, M, 2048, 1024, seed=5)
     packed = pack(tf, d)
