@@ -76,14 +76,16 @@ __device__ __forceinline__ void mfma_hazard_gap() {
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7");
 }
 
-// Workgroup barrier that waits only for this wave's LDS writes, not for the
-// kLead fragment reads issued after them (LDS operations complete in order,
-// so lgkmcnt <= 4 means every earlier one, the writes included, is done):
-// the reads stay in flight across the barrier.  s_waitcnt fields: vmcnt and
-// expcnt at their maximum (no wait), lgkmcnt = 4.
-__device__ __forceinline__ void barrier_after_writes() {
+// End-of-step barrier.  The A tile of a step reaches LDS by direct
+// global-to-LDS loads (four per thread, the last vector-memory operations of
+// every step); waiting until at most four are outstanding means that all but
+// this step's four -- among them those of the previous step, whose tile is
+// read from the next step on -- have landed.  LDS reads issued before the
+// barrier stay in flight (no LDS wait).  s_waitcnt fields: vmcnt = 4, expcnt
+// and lgkmcnt at their maximum (no wait).
+__device__ __forceinline__ void barrier_after_a_loads() {
     __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(0xC07F | (4 << 8));
+    __builtin_amdgcn_s_waitcnt(0x0F74);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
 }
@@ -121,7 +123,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     constexpr int T = PW / 16;                 // columns per lane per atom
     constexpr int PANELS = 64 / PW;            // panels per wave
     constexpr int SPG = kCS / MPC;             // steps per metadata group
-    __shared__ __align__(16) u32x4 As[kABufs][kBM * kBK / 8];
+    // One array per A buffer, so the compiler can tell the buffers apart when
+    // it orders LDS reads after the direct loads into another buffer.
+    __shared__ __align__(16) u32x4 As0[kBM * kBK / 8], As1[kBM * kBK / 8], As2[kBM * kBK / 8],
+        As3[kBM * kBK / 8];
+    auto abuf = [&](int j) -> u32x4* { return j == 0 ? As0 : j == 1 ? As1 : j == 2 ? As2 : As3; };
     __shared__ int last_flag;
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -132,20 +138,20 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     const int chunks = steps / kCS;            // the launcher requires K % 128 == 0
     constexpr int kDqSteps = BITS == 4 ? kDqW4Steps : kDqW8Steps;
 
+    // A step tile (256 rows x 32 halves = 1024 16-byte slots) arrives by four
+    // direct loads per thread; load r of wave w fills slots (4 w + r) * 64 +
+    // lane (a direct load writes lane l's 16 bytes at its base + 16 l), so
+    // each lane fetches the A chunk that belongs in its slot: slot X holds
+    // row X / 4, chunk (X % 4) ^ ((row / 4) % 4) (the inverse of a_slot).
     uint32_t avoff[4];
-    int aslot[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const int idx = tid + kThreads * r;
-        avoff[r] = (uint32_t)(idx >> 2) * (uint32_t)K * 2u + (uint32_t)(idx & 3) * 16u;
-        aslot[r] = a_slot(idx >> 2, idx & 3);
+        const int x = (4 * wave + r) * 64 + lane;
+        const int row = x >> 2, chk = (x & 3) ^ ((row >> 2) & 3);
+        avoff[r] = (uint32_t)row * (uint32_t)K * 2u + (uint32_t)chk * 16u;
     }
-    auto store_a = [&](int buf, const u32x4 (&av)[4]) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) As[buf][aslot[r]] = av[r];
-    };
     auto read_a = [&](int buf, int i) {
-        return __builtin_bit_cast(half8_t, As[buf][a_slot(16 * i + c, kg)]);
+        return __builtin_bit_cast(half8_t, abuf(buf)[a_slot(16 * i + c, kg)]);
     };
     struct Meta {
         uint32_t s[MPC][PANELS][(T + 1) / 2];   // T fp16 scales per group and panel
@@ -192,7 +198,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     // row m = 16 i + c, columns n = 16 t + 4 kg + 0..3 of the wave's tile.
     // The caller has made sure no wave still reads the A buffers underneath.
     auto store_tile = [&](int64_t row0, int64_t col0, auto&& get) {
-        uint8_t* stage = reinterpret_cast<uint8_t*>(&As[0][0]) + wave * 4096;
+        uint8_t* stage = reinterpret_cast<uint8_t*>(As0) + wave * 4096;
         constexpr int kStageRow = 144;
         const bool interior = row0 + kBM <= M && col0 + 64 <= N;
         const int rr = lane >> 3, cc = lane & 7;      // read-back: row rr (+8), 16-byte chunk cc
@@ -236,10 +242,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         // x 32 halves per step = 1024 16-byte chunks, 4 per thread.
         const int rows = (int)min<int64_t>(kBM, (int64_t)M - row0);
         const __amdgpu_buffer_rsrc_t a_rsrc = make_rsrc(A + row0 * K, (uint32_t)rows * (uint32_t)K * 2u);
-        auto load_a = [&](int step, u32x4 (&av)[4]) {
+        auto dma_a = [&](int step, int buf, int r) {      // direct load r of step's A tile
             const uint32_t soff = (uint32_t)min(step, steps - 1) * (kBK * 2);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) av[r] = load16(a_rsrc, avoff[r], soff);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                a_rsrc, (__attribute__((address_space(3))) void*)(abuf(buf) + (4 * wave + r) * 64), 16,
+                avoff[r], soff, 0, 0);
         };
         // B: packed panels and metadata as buffers; a panel past N is an
         // empty buffer (reads zero; its columns are never stored).
@@ -286,18 +293,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
 #pragma unroll
             for (int t = 0; t < 4; ++t) acc[i][t] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-        // Prologue (s0 = first step): A of steps s0, s0+1 in LDS, A of s0+2,
-        // s0+3 in flight; atoms of steps s0..s0+3 and metadata of the first
-        // two chunks requested; B operands of step s0; the first A fragments
-        // of step s0 read.  A register set j holds the A of a step = j mod 4.
+        // Prologue (s0 = first step): A of steps s0..s0+2 into LDS buffers
+        // 0..2; atoms of steps s0..s0+3 and metadata of the first two chunks
+        // requested; B operands of step s0; everything landed, then the first
+        // A fragments of step s0 read.  Buffer j holds the A of a step = j
+        // mod 4 (s0 is a multiple of 4).
         const int s0 = c0 * kCS;
-        u32x4 ra[kCS][4];
-        load_a(s0, ra[0]);
-        store_a(0, ra[0]);
-        load_a(s0 + 1, ra[1]);
-        store_a(1, ra[1]);
-        load_a(s0 + 2, ra[2]);
-        load_a(s0 + 3, ra[3]);
+#pragma unroll
+        for (int b = 0; b < 3; ++b)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dma_a(s0 + b, b, r);
 #pragma unroll
         for (int j = 0; j < kCS; ++j) load_atom(s0 + j, ring[j]);
         Meta mcur, mnext;
@@ -307,6 +312,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         make_consts(mcur, 0, kc);
         half8_t bop[4];
         dequant(ring[0], kc, bop);
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         // A fragment ring: block i of every step uses entry i % 8 (16 blocks
         // per step, so the pattern repeats exactly from step to step); reads
@@ -320,10 +326,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         // One K step s (j = s mod 4), as 64 MFMA slots (row block i = slot / 4,
         // column block t = slot % 4), each followed by at most one other
         // instruction group, fixed by scheduling fences:
-        //   slot 0        loads of A for step s+4 (into register set j, free
-        //                 since A of step s went to LDS during step s-2) and of
-        //                 the atoms for step s+4 (into the ring slot of step s,
-        //                 whose operands were formed during step s-1)
+        //   slot 0        loads of the atoms for step s+4 (into the ring slot
+        //                 of step s, whose operands were formed during s-1)
+        //   slots 2+4r    direct load r (0..3) of A of step s+3 into buffer
+        //                 (s+3) % 4, last read during step s-1 (before the
+        //                 previous barrier)
         //   slots 4i      A fragment of row block i + 4 from LDS (eight-entry
         //                 ring, so each LDS read has four blocks to land); for
         //                 i = 12..15 fragment i - 12 of step s+1 instead
@@ -331,11 +338,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         //   slots 4..55   the 52 (4-bit) or 48 (8-bit) dequantization
         //                 micro-steps of step s+1's B operands, one vector
         //                 instruction each, issued while the matrix core works
-        //   slots 40..43  A of step s+2 written to LDS (buffer last read in step
-        //                 s-2, before an earlier barrier); these writes come
-        //                 before the reads for step s+1, so the barrier's wait
-        //                 for "all but the last four LDS operations" covers them
-        // then one barrier, which waits for this wave's LDS writes only.
+        // then one barrier, after this wave's direct loads of step s+2 (issued
+        // during step s-1) have landed.
         for (int ch = c0; ch < c1; ++ch) {
 #pragma unroll
             for (int j = 0; j < kCS; ++j) {
@@ -355,10 +359,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                     const int i = q / 4, t = q % 4;
                     __builtin_amdgcn_sched_barrier(0);
                     mfma_acc(acc[i][t], bop[t], af[i % kRing]);
-                    if (q == 0) {
-                        load_a(step + 4, ra[j]);
-                        load_atom(step + 4, ring[j]);
-                    }
+                    if (q == 0) load_atom(step + 4, ring[j]);
+                    if (q % 4 == 2 && q < 16) dma_a(step + 3, (j + 3) % kABufs, q / 4);
                     if (t == 0 && i + kLead < kRB) af[(i + kLead) % kRing] = read_a(buf, i + kLead);
                     if (t == 0 && i + kLead >= kRB)
                         af[i + kLead - kRB] = read_a((j + 1) % kABufs, i + kLead - kRB);
@@ -367,18 +369,15 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                         dq_step(u, k, ring[(j + 1) % kCS], kc, st[u]);
                         if (k == kDqSteps - 1) bnext[u] = __builtin_bit_cast(half8_t, st[u].out);
                     }
-                    if (q >= 40 && q < 44) {
-                        const int r = q - 40;
-                        As[(j + 2) % kABufs][aslot[r]] = ra[(j + 2) % kCS][r];
-                    }
                 }
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int t = 0; t < 4; ++t) bop[t] = bnext[t];
-                barrier_after_writes();
+                barrier_after_a_loads();
             }
         }
         mfma_hazard_gap();
+        __builtin_amdgcn_s_waitcnt(0);   // direct loads issued for steps past the segment have landed
         __syncthreads();   // every wave done with the A buffers (the output staging reuses them)
     };
 
