@@ -227,8 +227,9 @@ def main():
             "peak": PEAK_F16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(tflops / PEAK_F16_TFLOPS, 4),
-            "traffic": recorded_traffic("tf_gemm.hip"),
-            "kernel": "gemm_kernel<4,1> (both prefill shapes)",
+            "traffic": recorded_traffic("tf_gemm256.hip"),
+            "kernel": "gemm256_kernel<4,1> (K=4096 N=14336: whole 256x256 tiles; "
+                      "K=14336 N=4096: stream-K over 256 blocks)",
         },
         "gemv": {
             "value": round(gemv_gbs, 1),
