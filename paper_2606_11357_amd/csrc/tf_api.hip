@@ -19,7 +19,7 @@ int check_weight(int bits, int64_t K, int64_t N, int group) {
 
 // Bytes of workspace the matmul kernels of this problem can use.
 int64_t workspace_bytes(const Layout& L, int64_t M) {
-    return M <= TF_GEMV_MAX_M ? tf::gemv_workspace_bytes(L, M) : tf::gemm_workspace_bytes(L, M);
+    return M <= tf::kSkinnyMaxM ? tf::gemv_workspace_bytes(L, M) : tf::gemm_workspace_bytes(L, M);
 }
 
 int check_matmul(int bits, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
@@ -49,7 +49,7 @@ int gemm_entry(int bits, const uint16_t* A, const void* packed, uint16_t* C, int
     rc = check_workspace(L, M, ws, ws_bytes);
     if (rc) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (M <= TF_GEMV_MAX_M) return tf::launch_gemv(L, A, packed, C, M, ws, s);
+    if (M <= tf::kSkinnyMaxM) return tf::launch_gemv(L, A, packed, C, M, ws, s);
     return tf::launch_gemm(L, A, packed, C, M, ws, ws_bytes, s);
 }
 

@@ -1,7 +1,10 @@
 // Decode GEMV (Section 2.1: batch-1 generation makes linear layers
 // matrix-vector products; Section 4.3 "GEMV microkernel"; Section 4.4).
 //
-// y[m, n] = sum_k x[m, k] * s[g, n] * (q[k, n] - z[g, n]),  1 <= M <= 8.
+// y[m, n] = sum_k x[m, k] * s[g, n] * (q[k, n] - z[g, n]),  1 <= M <= 8; the
+// same kernel with 16 row slots also serves the GEMM entry points for
+// 9 <= M <= 16 (skinny prefill), where the weights, not the matrix cores,
+// bound the time.
 //
 // Mapping (the GPU form of the principle of Section 4.4: every compute unit
 // streams its own weight slice, the activations are shared, each workgroup
@@ -58,7 +61,9 @@ template <int BITS, int M, int WAVES, int U, int APG>
 __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
     int K, int N, int group, int64_t s_off, int64_t z_off, int na, int ng, int S, int AS,
-    float* __restrict__ ws_part, uint32_t* __restrict__ ws_cnt) {
+    float* __restrict__ ws_part, uint32_t* __restrict__ ws_cnt, int mr) {
+    // mr <= M rows of A and C exist; row slots past them re-read row mr - 1
+    // (in bounds) and are never stored.
     using Cfg = GemvCfg<BITS, M, WAVES, U>;
     static_assert(APG == 0 || U % APG == 0, "a wave's run must hold whole groups");
     constexpr int T = Cfg::T, PW = Cfg::PW, RA = Cfg::ROUND_ATOMS;
@@ -110,7 +115,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 #pragma unroll
         for (int m = 0; m < M; ++m) {
             const int k = min(k0 + 4 * lane, K - 4);
-            b.xr[m] = *reinterpret_cast<const uint64_t*>(A + (int64_t)m * K + k);
+            b.xr[m] = *reinterpret_cast<const uint64_t*>(A + (int64_t)min(m, mr - 1) * K + k);
         }
         const int g0 = min(a0, na - 1) / apg;
         b.sr = *reinterpret_cast<const u32x4*>(spanel + min((int64_t)g0 * PW * 2 + 16 * lane, s_last));
@@ -299,7 +304,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         for (int i = tid; i < M * PW; i += NT) {
             const int m = i / PW, col = i % PW;
             const int n = p * PW + col;
-            if (n < N) {
+            if (n < N && m < mr) {
                 float v = 0.f;
 #pragma unroll
                 for (int w = 0; w < WAVES; ++w) v += sm.red[w][m][col];
@@ -338,7 +343,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         float v = 0.f;
         for (int s2 = 0; s2 < S; ++s2)
             v += __hip_atomic_load(&part[s2 * M * PW + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (n < N) C[(int64_t)m * N + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
+        if (n < N && m < mr) C[(int64_t)m * N + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
     }
     if (tid == 0)   // leave the counter at zero for the next call
         __hip_atomic_store(&ws_cnt[p], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -382,7 +387,7 @@ inline GemvPlan plan_gemv(const Layout& L, int64_t M) {
 
 template <int BITS, int M, int APG>
 int launch_g(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, void* ws,
-             hipStream_t s) {
+             int mr, hipStream_t s) {
     constexpr int WAVES = M == 1 ? 16 : 8;
     const GemvPlan sp = plan_gemv(L, M);
     const bool split = ws != nullptr && sp.S > 1;
@@ -392,15 +397,15 @@ int launch_g(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C,
     const int AS = split ? sp.AS : (int)L.na;
     return launch(gemv_kernel<BITS, M, WAVES, kGemvU, APG>, dim3((unsigned)L.np, (unsigned)S),
                   dim3(WAVES * 64), 0, s, A, pk, C, (int)L.K, (int)L.N, L.group, L.s_off, L.z_off,
-                  (int)L.na, (int)L.ng, S, AS, part, cnt);
+                  (int)L.na, (int)L.ng, S, AS, part, cnt, mr);
 }
 
 template <int BITS, int M>
 int launch_m(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, void* ws,
-             hipStream_t s) {
+             hipStream_t s, int mr = M) {
     // group 128 (the AWQ default) gets group boundaries fixed at compile time
-    if (L.group == 128) return launch_g<BITS, M, 4>(L, A, pk, C, ws, s);
-    return launch_g<BITS, M, 0>(L, A, pk, C, ws, s);
+    if (L.group == 128) return launch_g<BITS, M, 4>(L, A, pk, C, ws, mr, s);
+    return launch_g<BITS, M, 0>(L, A, pk, C, ws, mr, s);
 }
 
 template <int BITS>
@@ -417,16 +422,18 @@ int launch_bits(const Layout& L, const uint16_t* A, const void* packed, uint16_t
         case 7: return launch_m<BITS, 7>(L, A, pk, C, ws, s);
         case 8: return launch_m<BITS, 8>(L, A, pk, C, ws, s);
     }
+    if (M <= kSkinnyMaxM) return launch_m<BITS, kSkinnyMaxM>(L, A, pk, C, ws, s, (int)M);
     return TF_ERR_ARG;
 }
 
 }  // namespace
 
 int64_t gemv_workspace_bytes(const Layout& L, int64_t M) {
-    if (M < 1 || M > TF_GEMV_MAX_M) return 0;
-    const GemvPlan sp = plan_gemv(L, M);
+    if (M < 1 || M > kSkinnyMaxM) return 0;
+    const int64_t slots = M <= TF_GEMV_MAX_M ? M : kSkinnyMaxM;    // row slots of the kernel
+    const GemvPlan sp = plan_gemv(L, slots);
     if (sp.S <= 1) return 0;
-    return kWsCounterBytes + align256((int64_t)L.np * sp.S * M * L.pw * 4);
+    return kWsCounterBytes + align256((int64_t)L.np * sp.S * slots * L.pw * 4);
 }
 
 int launch_gemv(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,

@@ -48,6 +48,8 @@ constexpr int kLayoutVersion = 1;
 constexpr int64_t kWsCounterBytes = (TF_MAX_DIM / 32) * 4;
 // Most workgroups a stream-K GEMM launch uses (sizes its workspace).
 constexpr int kSkMaxGroups = 256;
+// GEMM calls with up to this many rows run the GEMV kernel (16 row slots).
+constexpr int kSkinnyMaxM = 16;
 constexpr int kAtomK = 32;
 constexpr int kAtomBytes = 1024;
 

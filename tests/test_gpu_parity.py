@@ -161,7 +161,8 @@ GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 2
                (4, 257, 768, 1000, 256), (8, 129, 1024, 200, 1024), (4, 96, 1152, 392, 96),
                (4, 600, 1024, 1040, 128), (8, 520, 512, 776, 64), (4, 513, 256, 2056, 32),
                (4, 1100, 512, 1040, 128), (8, 1030, 512, 776, 64), (4, 1280, 256, 520, 32),
-               (8, 1025, 1024, 264, 1024), (4, 1024, 640, 2048, 64)]
+               (8, 1025, 1024, 264, 1024), (4, 1024, 640, 2048, 64),
+               (4, 12, 1024, 200, 64), (8, 16, 2048, 264, 128), (4, 13, 512, 1032, 32), (8, 10, 384, 40, 128)]
 
 
 @pytest.mark.parametrize("bits,M,K,N,G", GEMM_SHAPES)
@@ -246,7 +247,8 @@ def test_workspace_shared_across_shapes(tf):
                       f"shared workspace, case {i}: W{bits} {M}x{K}x{N}")
 
 
-@pytest.mark.parametrize("bits,M,K,N,G", [(4, 1300, 2048, 1000, 128), (8, 1520, 1024, 776, 64),
+@pytest.mark.parametrize("bits,M,K,N,G", [(4, 16, 2048, 2048, 128), (8, 11, 4096, 520, 64),
+                                           (4, 1300, 2048, 1000, 128), (8, 1520, 1024, 776, 64),
                                            (4, 2048, 1024, 4096, 32), (4, 1100, 3072, 2320, 128)])
 def test_gemm_workspace_modes(tf, bits, M, K, N, G):
     """The stream-K split (workspace) and the whole-tile kernels (no workspace)
