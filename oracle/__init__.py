@@ -6,10 +6,12 @@ benchmark's CPU-baseline leg, never by the library.
 from .awq_oracle import (  # noqa: F401
     dequant,
     dequant_f16,
+    dequant_sym,
     group_of,
     matmul,
     to_f16,
     unpack_w4,
     w4a16,
     w8a16,
+    w8a16_sym,
 )

@@ -17,6 +17,9 @@ steps changes where they run, not the mathematics -- Sections 1 and 4.1.1):
                (Section 2.2; Section 4.2 metadata paragraph, G = 128).
 3. dequant  -- w_hat = s_g * (q - z_g)                 (Section 2.2, Eq. 2);
                the symmetric form w_hat = s_g * q (Eq. 1) is the case z = 0.
+               The paper's own W8A16 is symmetric, signed INT8, one scale per
+               output channel (Section 2.2, last paragraph; Section 4.3):
+               w_hat[k, n] = s[n] * q[k, n]  (dequant_sym).
 4. matmul   -- C = A x B with A [M, K], B [K, N] the dequantized weights
                (Section 2.1 problem statement), accumulated in float64.
 5. output   -- round-to-nearest-even to fp16 (the library's output dtype).
@@ -40,6 +43,8 @@ __all__ = [
     "to_f16",
     "w4a16",
     "w8a16",
+    "dequant_sym",
+    "w8a16_sym",
 ]
 
 
@@ -112,3 +117,20 @@ def w8a16(x: np.ndarray, qweight: np.ndarray, zeros: np.ndarray, scales: np.ndar
     """Full W8A16 result in float64: the byte is the code -> dequant (Eq. 2) -> matmul."""
     return matmul(x, dequant(np.asarray(qweight, dtype=np.uint8),
                              np.asarray(zeros, dtype=np.uint8), scales, group))
+
+
+def dequant_sym(q: np.ndarray, s: np.ndarray) -> np.ndarray:
+    """Eq. 1 with one scale per output channel: ``w_hat[k, n] = s[n] * q[k, n]``.
+
+    ``q`` is signed INT8 ``[K, N]``, ``s`` fp16 ``[N]`` (Section 2.2, W8A16 with
+    per-channel symmetric quantization and no zero-points; Section 4.3, the
+    INT8 value times the channel's scale).  float64; exact, as in ``dequant``.
+    """
+    q = np.asarray(q).astype(np.float64)
+    s = np.asarray(s).astype(np.float64)
+    return s[None, :] * q
+
+
+def w8a16_sym(x: np.ndarray, qweight: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """Full symmetric per-channel W8A16 result in float64: dequant (Eq. 1) -> matmul."""
+    return matmul(x, dequant_sym(np.asarray(qweight, dtype=np.int8), scales))

@@ -31,6 +31,7 @@ import numpy as np
 __all__ = [
     "pack_nibbles",
     "make_inputs",
+    "make_inputs_w8sym",
     "WORKLOADS",
 ]
 
@@ -84,6 +85,21 @@ def make_inputs(bits: int, M: int, K: int, N: int, group: int = 128, seed: int =
         out["qweight"] = q
         out["zeros"] = z
     return out
+
+
+def make_inputs_w8sym(M: int, K: int, N: int, seed: int = 0, x_std: float = 1.0,
+                      s_lo: float = 0.0003, s_hi: float = 0.001) -> dict:
+    """Draw one seeded per-channel symmetric INT8 workload (the paper's W8A16).
+
+    Draw order x -> q -> s: ``x`` fp16 ``[M, K]`` as in ``make_inputs``; ``q``
+    uniform signed integers in ``[-128, 127]``, int8 ``[K, N]``; ``s`` uniform in
+    ``[s_lo, s_hi]`` drawn in float64 then rounded to fp16, one per column ``[N]``.
+    """
+    rng = np.random.default_rng(seed)
+    x = (x_std * rng.standard_normal((M, K))).astype(np.float16)
+    q = rng.integers(-128, 128, size=(K, N), dtype=np.int8)
+    s = rng.uniform(s_lo, s_hi, size=(N,)).astype(np.float16)
+    return {"M": M, "K": K, "N": N, "x": x, "q": q, "s": s, "qweight": q, "scales": s}
 
 
 # The synthetic Llama-shaped workloads the library is measured and checked on.
