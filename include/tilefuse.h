@@ -101,6 +101,23 @@ int tf_pack_w8(const uint8_t* qweight, const uint8_t* zeros, const uint16_t* sca
                int64_t K, int64_t N, int group, void* packed, void* stream);
 
 /*
+ * Offline pre-tiling of the W8A16 form of Section 2.2 (W8A16 paragraph):
+ * signed INT8 weights with one scale per output channel and no zero-point,
+ * dequantized by Eq. 1 as w_hat[k, n] = s[n] * q[k, n].
+ *   qweight  int8  [K, N]     q[k, n] in -128..127
+ *   scales   fp16  [N]        s[n]
+ *   packed   tf_packed_bytes(8, K, N, group) bytes
+ * Stored as the 8-bit layout with codes q + 128, zero-point 128 and the
+ * column's scale repeated in every group of `group` rows, so the 8-bit
+ * matmul and debug entry points (bits = 8, the same group) apply unchanged:
+ * s * ((q + 128) - 128) = s * q exactly.  `group` only sets that internal
+ * grouping (128 is the usual choice; it needs K % group == 0).  Same
+ * constraints and errors as tf_pack_w8.
+ */
+int tf_pack_w8_sym(const int8_t* qweight, const uint16_t* scales, int64_t K, int64_t N, int group,
+                   void* packed, void* stream);
+
+/*
  * Workspace the matmul entry points can use for this problem, in bytes (0
  * when the kernels chosen for it need none).  Negative tf_status on bad
  * arguments.  The workspace holds per-K-slice partial sums and arrival

@@ -111,6 +111,16 @@ int tf_pack_w8(const uint8_t* qweight, const uint8_t* zeros, const uint16_t* sca
                               static_cast<hipStream_t>(stream));
 }
 
+int tf_pack_w8_sym(const int8_t* qweight, const uint16_t* scales, int64_t K, int64_t N, int group,
+                   void* packed, void* stream) {
+    if (!qweight || !scales || !packed) return TF_ERR_NULL;
+    int rc = check_weight(8, K, N, group);
+    if (rc) return rc;
+    if (misaligned(qweight) || misaligned(scales) || misaligned(packed)) return TF_ERR_ALIGN;
+    return tf::launch_pack_w8_sym(qweight, scales, tf::make_layout(8, K, N, group), packed,
+                                  static_cast<hipStream_t>(stream));
+}
+
 int64_t tf_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group) {
     int rc = check_weight(bits, K, N, group);
     if (rc) return rc;

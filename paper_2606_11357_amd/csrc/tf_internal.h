@@ -269,6 +269,8 @@ int launch_pack_w4(const int32_t* qw, const int32_t* qz, const uint16_t* sc, con
                    void* packed, hipStream_t s);
 int launch_pack_w8(const uint8_t* qw, const uint8_t* zr, const uint16_t* sc, const Layout& L,
                    void* packed, hipStream_t s);
+int launch_pack_w8_sym(const int8_t* qw, const uint16_t* sc, const Layout& L, void* packed,
+                       hipStream_t s);
 int launch_unpack(const Layout& L, const void* packed, uint8_t* q_out, uint8_t* z_out,
                   hipStream_t s);
 int launch_dequant(const Layout& L, const void* packed, int out_dtype, void* w_out,

@@ -34,8 +34,11 @@ __global__ void pack_w4_weights(const int32_t* __restrict__ qw, uint32_t* __rest
     out[d] = word;
 }
 
+// flip = 0x80808080 turns signed INT8 codes into unsigned codes q + 128
+// (two's complement: flipping the sign bit adds 128).
 __global__ void pack_w8_weights(const uint8_t* __restrict__ qw, uint32_t* __restrict__ out,
-                                int64_t K, int64_t N, int64_t na, int64_t total_dwords) {
+                                int64_t K, int64_t N, int64_t na, int64_t total_dwords,
+                                uint32_t flip) {
     int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (d >= total_dwords) return;
     int64_t atom = d >> 8;
@@ -48,16 +51,18 @@ __global__ void pack_w8_weights(const uint8_t* __restrict__ qw, uint32_t* __rest
     if (n < N) {
         int64_t k0 = a * kAtomK + 8 * kg + 4 * (t & 1);
         for (int b = 0; b < 4; ++b) word |= (uint32_t)qw[(k0 + b) * N + n] << (8 * b);
+        word ^= flip;
     }
     out[d] = word;
 }
 
 // One thread per metadata entry: scales copied bit for bit, zero-points
-// unpacked to one byte each.
+// unpacked to one byte each.  s_gstride = N for per-group scales [K/G, N], 0
+// for one scale per column [N]; with neither zero-point array, zconst.
 __global__ void pack_meta(const uint16_t* __restrict__ sc, const int32_t* __restrict__ qz4,
                           const uint8_t* __restrict__ z8, uint16_t* __restrict__ s_out,
                           uint8_t* __restrict__ z_out, int64_t N, int64_t ng, int pw,
-                          int64_t entries) {
+                          int64_t entries, int64_t s_gstride, int zconst) {
     int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= entries) return;
     int64_t p = e / (ng * pw);
@@ -69,12 +74,14 @@ __global__ void pack_meta(const uint16_t* __restrict__ sc, const int32_t* __rest
     uint16_t s = 0;
     uint8_t z = 0;
     if (n < N) {
-        s = sc[g * N + n];
+        s = sc[g * s_gstride + n];
         if (qz4) {
             uint32_t w = reinterpret_cast<const uint32_t*>(qz4)[g * (N / 8) + (n >> 3)];
             z = (uint8_t)((w >> (4 * (int)(n & 7))) & 0xFu);
-        } else {
+        } else if (z8) {
             z = z8[g * N + n];
+        } else {
+            z = (uint8_t)zconst;
         }
     }
     s_out[e] = s;
@@ -206,7 +213,7 @@ int launch_pack_w4(const int32_t* qw, const int32_t* qz, const uint16_t* sc, con
     int64_t entries = L.np * L.ng * L.pw;
     return launch(pack_meta, dim3(blocks_for(entries, 256)), dim3(256), 0, s, sc, qz,
                   (const uint8_t*)nullptr, reinterpret_cast<uint16_t*>(base + L.s_off),
-                  base + L.z_off, L.N, L.ng, (int)L.pw, entries);
+                  base + L.z_off, L.N, L.ng, (int)L.pw, entries, L.N, 0);
 }
 
 int launch_pack_w8(const uint8_t* qw, const uint8_t* zr, const uint16_t* sc, const Layout& L,
@@ -214,12 +221,30 @@ int launch_pack_w8(const uint8_t* qw, const uint8_t* zr, const uint16_t* sc, con
     uint8_t* base = static_cast<uint8_t*>(packed);
     int64_t dwords = L.np * L.na * 256;
     int rc = launch(pack_w8_weights, dim3(blocks_for(dwords, 256)), dim3(256), 0, s, qw,
-                    reinterpret_cast<uint32_t*>(base + L.w_off), L.K, L.N, L.na, dwords);
+                    reinterpret_cast<uint32_t*>(base + L.w_off), L.K, L.N, L.na, dwords, 0u);
     if (rc) return rc;
     int64_t entries = L.np * L.ng * L.pw;
     return launch(pack_meta, dim3(blocks_for(entries, 256)), dim3(256), 0, s, sc,
                   (const int32_t*)nullptr, zr, reinterpret_cast<uint16_t*>(base + L.s_off),
-                  base + L.z_off, L.N, L.ng, (int)L.pw, entries);
+                  base + L.z_off, L.N, L.ng, (int)L.pw, entries, L.N, 0);
+}
+
+// Signed INT8 with one scale per column (Eq. 1): stored as the 8-bit layout
+// with codes q + 128, zero-point 128 and the column's scale in every group,
+// so s * ((q + 128) - 128) = s * q through the same kernels.
+int launch_pack_w8_sym(const int8_t* qw, const uint16_t* sc, const Layout& L, void* packed,
+                       hipStream_t s) {
+    uint8_t* base = static_cast<uint8_t*>(packed);
+    int64_t dwords = L.np * L.na * 256;
+    int rc = launch(pack_w8_weights, dim3(blocks_for(dwords, 256)), dim3(256), 0, s,
+                    reinterpret_cast<const uint8_t*>(qw), reinterpret_cast<uint32_t*>(base + L.w_off),
+                    L.K, L.N, L.na, dwords, 0x80808080u);
+    if (rc) return rc;
+    int64_t entries = L.np * L.ng * L.pw;
+    return launch(pack_meta, dim3(blocks_for(entries, 256)), dim3(256), 0, s, sc,
+                  (const int32_t*)nullptr, (const uint8_t*)nullptr,
+                  reinterpret_cast<uint16_t*>(base + L.s_off), base + L.z_off, L.N, L.ng, (int)L.pw,
+                  entries, (int64_t)0, 128);
 }
 
 int launch_unpack(const Layout& L, const void* packed, uint8_t* q_out, uint8_t* z_out,

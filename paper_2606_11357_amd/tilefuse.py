@@ -26,7 +26,7 @@ GEMV_MAX_M = 8
 
 EXPORTS = (
     "tf_layout_version", "tf_status_str", "tf_packed_bytes", "tf_pack_w4", "tf_pack_w8",
-    "tf_workspace_bytes", "tf_w4a16_gemm", "tf_w8a16_gemm", "tf_w4a16_gemv",
+    "tf_pack_w8_sym", "tf_workspace_bytes", "tf_w4a16_gemm", "tf_w8a16_gemm", "tf_w4a16_gemv",
     "tf_w8a16_gemv", "tf_unpack", "tf_dequant",
 )
 
@@ -56,6 +56,7 @@ def load() -> ctypes.CDLL:
         "tf_packed_bytes": (I64, [I, I64, I64, I]),
         "tf_pack_w4": (I, [P, P, P, I64, I64, I, P, P]),
         "tf_pack_w8": (I, [P, P, P, I64, I64, I, P, P]),
+        "tf_pack_w8_sym": (I, [P, P, I64, I64, I, P, P]),
         "tf_workspace_bytes": (I64, [I, I64, I64, I64, I]),
         "tf_w4a16_gemm": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_w8a16_gemm": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
@@ -159,6 +160,18 @@ def pack_w8(qweight, zeros, scales, K: int, N: int, group: int = 128, out=None):
         out = torch.empty(packed_bytes(8, K, N, group), dtype=torch.uint8, device=qweight.device)
     _check(load().tf_pack_w8(_ptr(qweight), _ptr(zeros), _ptr(scales), K, N, group, _ptr(out),
                              _stream(qweight.device)), "tf_pack_w8")
+    return out
+
+
+def pack_w8_sym(qweight, scales, K: int, N: int, group: int = 128, out=None):
+    """Pre-tile a signed INT8 weight with one scale per output channel
+    (int8 [K, N], fp16 [N]); use it with the 8-bit matmul calls and `group`."""
+    torch = _torch()
+    _need_cuda(qweight, scales)
+    if out is None:
+        out = torch.empty(packed_bytes(8, K, N, group), dtype=torch.uint8, device=qweight.device)
+    _check(load().tf_pack_w8_sym(_ptr(qweight), _ptr(scales), K, N, group, _ptr(out),
+                                 _stream(qweight.device)), "tf_pack_w8_sym")
     return out
 
 

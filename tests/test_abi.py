@@ -175,6 +175,19 @@ def test_pack_rejects(lib):
         assert fn(P, P, P, 256, 64, 16, P, NULL) == tfb.TF_ERR_GROUP
 
 
+def test_pack_w8_sym_rejects(lib):
+    ok = (P, P, 256, 64, 128, P, NULL)
+    for i in (0, 1, 5):
+        a = list(ok)
+        a[i] = NULL
+        assert lib.tf_pack_w8_sym(*a) == tfb.TF_ERR_NULL
+        a[i] = P_ODD
+        assert lib.tf_pack_w8_sym(*a) == tfb.TF_ERR_ALIGN
+    assert lib.tf_pack_w8_sym(P, P, 256, 60, 128, P, NULL) == tfb.TF_ERR_SHAPE
+    assert lib.tf_pack_w8_sym(P, P, 200, 64, 128, P, NULL) == tfb.TF_ERR_SHAPE
+    assert lib.tf_pack_w8_sym(P, P, 256, 64, 16, P, NULL) == tfb.TF_ERR_GROUP
+
+
 def test_unpack_dequant_reject(lib):
     assert lib.tf_unpack(4, NULL, 256, 64, 128, P, P, NULL) == tfb.TF_ERR_NULL
     assert lib.tf_unpack(4, P, 256, 64, 128, NULL, P, NULL) == tfb.TF_ERR_NULL
