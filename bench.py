@@ -76,6 +76,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the step, time every synthetic workload configuration "
+                         "(one JSON line each)")
     return ap.parse_args()
 
 
@@ -124,6 +127,68 @@ def calibrate_copy(torch):
                       "bytes_written": COPY_BYTES, "launches": 3}), flush=True)
 
 
+def algo_bytes(bits, K, N, G=GROUP):
+    """Packed codes + fp16 scales + zero-points (4-bit packed, 8-bit as bytes)."""
+    if bits == 4:
+        return algo_bytes_w4(K, N, G)
+    return K * N + (K // G) * N * 2 + (K // G) * N
+
+
+def sweep(torch, tf, make_inputs, reps=50):
+    """Every workload of synth.WORKLOADS: HIP-event time per launch over
+    3 replays of a graph of `reps` launches rotating over enough distinct
+    copies of the packed weight that the copies exceed 512 MB (so weights
+    stream from HBM, not the MALL), the library's default workspace, inputs
+    resident."""
+    from paper_2606_11357_amd.synth import WORKLOADS
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    for name, (bits, Ms, K, N, xstd) in WORKLOADS.items():
+        for M in Ms:
+            d = make_inputs(bits, M, K, N, group=GROUP, seed=0, x_std=xstd)
+            if bits == 4:
+                p0 = tf.pack_w4(up(d["qweight"]), up(d["qzeros"]), up(d["s"]), K, N, GROUP)
+                fn = tf.w4a16_gemm
+            else:
+                p0 = tf.pack_w8(up(d["qweight"]), up(d["zeros"]), up(d["s"]), K, N, GROUP)
+                fn = tf.w8a16_gemm
+            ncopy = int(min(40, max(2, -(-(512 << 20) // p0.numel()))))
+            copies = [p0] + [p0.clone() for _ in range(ncopy - 1)]
+            x = up(d["x"])
+            y = torch.empty((M, N), dtype=torch.float16, device=dev)
+            for i in range(5):
+                fn(x, copies[i % ncopy], K, N, GROUP, out=y)
+            torch.cuda.synchronize()
+            # the launches are replayed from a HIP graph, so the host-side cost
+            # of a Python call does not leave the GPU idle between small kernels
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for i in range(reps):
+                    fn(x, copies[i % ncopy], K, N, GROUP, out=y)
+            g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(3):
+                g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / (3 * reps)
+            tflops = 2.0 * M * N * K / us / 1e6
+            gbs = algo_bytes(bits, K, N) / us / 1e3
+            hbm_bound = M <= 16
+            print(json.dumps({
+                "workload": name, "bits": bits, "M": M, "K": K, "N": N, "group": GROUP,
+                "us_per_launch": round(us, 3), "TFLOP/s": round(tflops, 2), "GB/s": round(gbs, 1),
+                "bound": "hbm" if hbm_bound else "mfma",
+                "frac": round(gbs / PEAK_HBM_GBS if hbm_bound else tflops / PEAK_F16_TFLOPS, 4),
+                "weight_copies": ncopy, "launches": 3 * reps, "timing": "HIP graph replay"}),
+                flush=True)
+            del g, copies, p0, x, y, d
+            torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -142,6 +207,9 @@ def main():
         calibrate_copy(torch)
         return
     tf.load()
+    if args.sweep:
+        sweep(torch, tf, make_inputs)
+        return
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
 

@@ -350,14 +350,19 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 }
 
 // Launch plan.  A workgroup of WAVES waves owns one panel and one K-slice of
-// AS atoms.  K is split only when the panels alone would leave much of the
-// chip idle (few output columns): splitting costs a partial-sum round trip,
-// which only pays when it adds many more busy compute units.
+// AS atoms.  K is split only when few panels (output columns) each carry much
+// work: the partial-sum round trip through the workspace (store, arrival
+// count, reload: a few microseconds of latency) pays only when it spreads a
+// long stream of atoms, or many rows of A, over more compute units.  The
+// work measure na * max(1, M / 2) and its threshold come from kernel-trace
+// timings of both forms on MI355X (e.g. K=4096 with 64 or 128 panels at M=1:
+// one pass is faster; K=14336 with 64 panels: the split is).
 struct GemvPlan {
     int waves, S, AS;
 };
 constexpr int kGemvU = 8, kMaxSplit = 32;
-constexpr int64_t kSplitBelowPanels = 192;   // split K only below this many panels
+constexpr int64_t kSplitBelowPanels = 192;      // split K only below this many panels ...
+constexpr int64_t kSplitFromWork = 256;         // ... carrying at least this much work each
 constexpr int64_t kTargetWorkgroups = 256;
 
 inline int gemv_waves(int64_t M) { return M == 1 ? 16 : 8; }
@@ -367,7 +372,7 @@ inline GemvPlan plan_gemv(const Layout& L, int64_t M) {
     const int64_t ra = (int64_t)waves * kGemvU;
     const int64_t apg = L.group / kAtomK;
     int64_t S = 1;
-    if (L.np < kSplitBelowPanels) {
+    if (L.np < kSplitBelowPanels && L.na * std::max<int64_t>(1, M / 2) >= kSplitFromWork) {
         S = (kTargetWorkgroups + L.np - 1) / L.np;
         S = std::min<int64_t>(S, (L.na + ra - 1) / ra);
         S = std::min<int64_t>(S, kMaxSplit);

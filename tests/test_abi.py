@@ -152,13 +152,13 @@ def test_workspace_query(lib):
 
 @pytest.mark.parametrize("bits", [4, 8])
 def test_workspace_rejects(lib, bits):
-    need = lib.tf_workspace_bytes(bits, 1, 14336, 4096, 128)
+    need = lib.tf_workspace_bytes(bits, 1, 14336, 2048, 128)
     assert need > 0
     fn = lib.tf_w4a16_gemv if bits == 4 else lib.tf_w8a16_gemv
-    assert fn(P, P, P, 1, 14336, 4096, 128, P, need - 16, NULL) == tfb.TF_ERR_ARG
-    assert fn(P, P, P, 1, 14336, 4096, 128, P_ODD, need, NULL) == tfb.TF_ERR_ALIGN
+    assert fn(P, P, P, 1, 14336, 2048, 128, P, need - 16, NULL) == tfb.TF_ERR_ARG
+    assert fn(P, P, P, 1, 14336, 2048, 128, P_ODD, need, NULL) == tfb.TF_ERR_ALIGN
     fn = lib.tf_w4a16_gemm if bits == 4 else lib.tf_w8a16_gemm
-    assert fn(P, P, P, 1, 14336, 4096, 128, P, need - 16, NULL) == tfb.TF_ERR_ARG
+    assert fn(P, P, P, 1, 14336, 2048, 128, P, need - 16, NULL) == tfb.TF_ERR_ARG
 
 
 def test_pack_rejects(lib):

@@ -217,7 +217,7 @@ def test_closed_form(tf):
 
 @pytest.mark.parametrize("bits,M,K,N", [(4, 1, 4096, 14336), (4, 1, 14336, 4096), (8, 1, 14336, 4096),
                                         (4, 3, 8192, 1000), (8, 8, 8192, 520), (4, 5, 32768, 136),
-                                        (4, 2, 256, 64), (8, 1, 4096, 4096)])
+                                        (4, 2, 256, 64), (8, 1, 4096, 4096), (8, 3, 14336, 2048)])
 def test_gemv_workspace_modes(tf, bits, M, K, N):
     """Split-K (workspace) and single-pass (no workspace) kernels both meet the
     bar, and a workspace can be reused at once."""
@@ -248,6 +248,7 @@ def test_workspace_shared_across_shapes(tf):
 
 
 @pytest.mark.parametrize("bits,M,K,N,G", [(4, 16, 2048, 2048, 128), (8, 11, 4096, 520, 64),
+                                           (4, 12, 16384, 512, 128), (8, 16, 14336, 1024, 128),
                                            (4, 1300, 2048, 1000, 128), (8, 1520, 1024, 776, 64),
                                            (4, 2048, 1024, 4096, 32), (4, 1100, 3072, 2320, 128)])
 def test_gemm_workspace_modes(tf, bits, M, K, N, G):
