@@ -12,18 +12,27 @@
 //  - a workgroup owns a panel of PW output columns and all of K, or, when the
 //    panels alone are too few to fill the chip and a workspace is given, one
 //    slice of K;
-//  - every wave first loads its slice of x and its groups' metadata, then all
-//    of its U weight atoms (one 16-byte load per lane per atom), and consumes
-//    the atoms in arrival order; x and metadata sit in wave-private LDS;
+//  - each wave streams a contiguous run of the slice's atoms (one 16-byte
+//    load per lane per atom) through a small ring of registers: the atom D
+//    places ahead is requested as each one is consumed.  Issuing a wave's
+//    whole share at once queues the entire transfer in the memory system
+//    within about a microsecond, and the first-needed bytes then arrive
+//    anywhere in it while the vector units wait;
+//  - the run is consumed in rounds of U atoms; a round's slice of x and its
+//    groups' metadata are loaded one round ahead and staged in wave-private
+//    LDS;
 //  - a lane owns T columns x 8 rows of an atom: one 16-byte activation slice
 //    per row of A feeds its T columns (the widening idea of Section 4.3: one
 //    activation fragment reused across many outputs).
 // Arithmetic (Eq. 2 summed over a group, where s and z are constant):
-//    sum_k x (s (q - z)) = s * (sum_k x q - z * sum_k x).
-//  - M < 4: codes are read as exact fp16 integers 1024 + q (or 1024 + 16 q,
-//    which needs no shift) and dotted with x by v_dot2_f32_f16; the offsets
-//    and z are removed per group with the per-lane sums of x.
-//  - M >= 4: each weight is dequantized once to fp16 with the GEMM's code,
+//    sum_k x (s (q - z)) = s * (sum_k x c - sum_k x o - z * sum_k x),
+// with c = o + q the code read as an exact fp16 integer and o its offset.
+//  - M <= 4 ("factored"): 4-bit codes are read as 1024 + q (rows 0,1,4,5 of a
+//    lane's 8) or 64 + q (rows 2,3,6,7), 8-bit codes as 1024 + q, and dotted
+//    with x by v_dot2_f32_f16 into one fp32 sum per column; the offsets and z
+//    are removed once per group with sums of x that each wave forms once per
+//    round for all of its columns.
+//  - M > 4: each weight is dequantized once to fp16 with the GEMM's code,
 //    RNE(s (q - z)), and dotted with all M rows of x.
 // All sums are fp32.  Lanes sharing a column combine by cross-lane shuffles,
 // the waves through LDS; K-slices through a workspace, added by the last
@@ -36,40 +45,45 @@
 namespace tf {
 namespace {
 
-template <int BITS, int M, int WAVES, int U>
+constexpr int kGemvU = 8;        // atoms per wave per round
+constexpr int kFactMaxM = 4;     // rows up to which the factored form runs
+
+template <int BITS, int M>
 struct GemvCfg {
     static constexpr int T = BITS == 4 ? 4 : 2;      // columns per lane
     static constexpr int PW = BITS == 4 ? 64 : 32;   // panel width
-    static constexpr int ROUND_ATOMS = WAVES * U;    // atoms of one round of the workgroup
-    static constexpr int XB = U * kAtomK * 2;        // bytes of one row of x per wave-round
-    static constexpr int SB = U * PW * 2;            // scale bytes of up to U groups
-    static constexpr int ZB = U * PW;                // zero-point bytes of up to U groups
-    static constexpr bool FACT = M < 4;
-    static_assert(XB == 512 && SB <= 1024 && ZB <= 512, "one cooperative load per lane each");
+    static constexpr bool FACT = M <= kFactMaxM;
 };
 
 // One wave's staging area in LDS (private to the wave: no barrier needed).
-template <int M, int U, int PW>
+template <int M, int PW>
 struct WaveStage {
-    uint64_t x[M][U * kAtomK / 4];     // M rows x U*32 halves
-    u32x4 s[U * PW * 2 / 16];
-    uint64_t z[U * PW / 8];
+    uint64_t x[M][64];                  // lane l holds k = 4l..4l+3 of the round's 256
+    float2_t cs[M][64];                 // factored form: lane l: sums of 8-k slice l / 2
+    u32x4 s[kGemvU * PW * 2 / 16];      // scales of up to U groups
+    uint64_t z[kGemvU * PW / 8];        // zero-points of up to U groups
 };
 
-// APG: atoms per group when known at compile time (4 for G = 128), else 0.
-template <int BITS, int M, int WAVES, int U, int APG>
+// SEG > 0: segments (atoms summed before the scale is applied) have SEG
+// atoms, fixed at compile time (one group of 32 SEG rows); SEG = 0: group
+// size known at run time.  D: weight atoms a wave keeps in flight.
+template <int BITS, int M, int WAVES, int SEG, int D>
 __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
-    int K, int N, int group, int64_t s_off, int64_t z_off, int na, int ng, int S, int AS,
+    int K, int N, int group, int64_t s_off, int64_t z_off, int na, int ng, int S, int AS, int RW,
     float* __restrict__ ws_part, uint32_t* __restrict__ ws_cnt, int mr) {
     // mr <= M rows of A and C exist; row slots past them re-read row mr - 1
     // (in bounds) and are never stored.
-    using Cfg = GemvCfg<BITS, M, WAVES, U>;
-    static_assert(APG == 0 || U % APG == 0, "a wave's run must hold whole groups");
-    constexpr int T = Cfg::T, PW = Cfg::PW, RA = Cfg::ROUND_ATOMS;
+    using Cfg = GemvCfg<BITS, M>;
+    constexpr int U = kGemvU, T = Cfg::T, PW = Cfg::PW;
     constexpr bool FACT = Cfg::FACT;
     constexpr int NT = WAVES * 64;
-    using Stage = WaveStage<M, U, PW>;
+    static_assert(SEG == 0 || U % SEG == 0, "segments tile a round");
+    static_assert(U % D == 0, "the load ring tiles a round");
+    // metadata of the groups one round touches: U / SEG groups, or up to U
+    constexpr int NGR = SEG > 0 ? U / SEG : U;
+    constexpr int SLANES = NGR * PW * 2 / 16, ZLANES = NGR * PW / 8;
+    using Stage = WaveStage<M, PW>;
     union Smem {
         Stage st[WAVES];
         float red[WAVES][M][PW];
@@ -78,20 +92,27 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 
     const int p = blockIdx.x;
     const int split = blockIdx.y;                       // K-slice of this workgroup
-    const int a_begin = split * AS;
-    const int a_end = min(na, a_begin + AS);
+    const int a_end = min(na, split * AS + AS);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar) index math
     const int c = lane & 15, kg = lane >> 4;
-    const int apg = APG > 0 ? APG : group / kAtomK;
+    const int apg = group / kAtomK;
     const uint32_t magic = magic_reg();
-    const u32x4* wpanel = reinterpret_cast<const u32x4*>(packed) + (int64_t)p * na * 64 + lane;
+    const uint32_t magic64 = magic64_reg();
+    // this wave's run: atoms aw0 .. aw_end-1 of the panel (RW per wave; a
+    // multiple of the group's atoms when SEG > 0)
+    const int aw0 = split * AS + wave * RW;
+    const int aw_end = min(a_end, aw0 + RW);
+    const int nw = aw_end - aw0;                        // may be <= 0: an idle wave
+    const int nrounds = nw > 0 ? (nw + U - 1) / U : 0;
+    const u32x4* wrun = reinterpret_cast<const u32x4*>(packed) + (int64_t)p * na * 64 + lane;
     const uint8_t* spanel = packed + s_off + (int64_t)p * ng * PW * 2;
     const uint8_t* zpanel = packed + z_off + (int64_t)p * ng * PW;
     const int64_t s_last = ((int64_t)ng * PW * 2 - 16);     // last 16-byte slot of the panel's scales
     const int64_t z_last = ((int64_t)ng * PW - 8);
-    const int rounds = (a_end - a_begin + RA - 1) / RA;
     Stage& st = sm.st[wave];
+    const uint8_t* sbytes = reinterpret_cast<const uint8_t*>(st.s);
+    const uint8_t* zbytes = reinterpret_cast<const uint8_t*>(st.z);
 
     float y[M][T];
 #pragma unroll
@@ -99,187 +120,213 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 #pragma unroll
         for (int t = 0; t < T; ++t) y[m][t] = 0.f;
 
-    // Loads of one round: first the wave's slice of x and its groups'
-    // metadata (small), then its U weight atoms.  Addresses are clamped into
-    // the panel so every load is in bounds and the code stays branch-free;
-    // atoms past K are skipped at use.
-    struct Buf {
+    // Loads.  A round is U atoms of the run; its small loads (the wave's
+    // slice of x, its groups' metadata) are issued one round ahead.  Weight
+    // atoms stream through a ring of D registers: the atom D places ahead is
+    // requested as each one is taken, so the memory queues stay short and
+    // data comes back in the order it is used (issuing everything at once
+    // lets the first-needed bytes arrive anywhere in the whole transfer).
+    // Addresses are clamped into the panel, so every load is in bounds.
+    struct Meta {
         uint64_t xr[M];
         u32x4 sr;
         uint64_t zr;
-        u32x4 w[U];
     };
-    auto issue = [&](int r, Buf& b) {
-        const int a0 = a_begin + r * RA + wave * U;
-        const int k0 = min(a0, na - 1) * kAtomK;
+    auto issue_meta = [&](int r, Meta& mt) {
+        const int ac = min(aw0 + r * U, na - 1);
+        const int k0 = ac * kAtomK;
 #pragma unroll
         for (int m = 0; m < M; ++m) {
             const int k = min(k0 + 4 * lane, K - 4);
-            b.xr[m] = *reinterpret_cast<const uint64_t*>(A + (int64_t)min(m, mr - 1) * K + k);
+            mt.xr[m] = *reinterpret_cast<const uint64_t*>(A + (int64_t)min(m, mr - 1) * K + k);
         }
-        const int g0 = min(a0, na - 1) / apg;
-        b.sr = *reinterpret_cast<const u32x4*>(spanel + min((int64_t)g0 * PW * 2 + 16 * lane, s_last));
-        b.zr = *reinterpret_cast<const uint64_t*>(zpanel + min((int64_t)g0 * PW + 8 * lane, z_last));
-#pragma unroll
-        for (int i = 0; i < U; ++i)
-            b.w[i] = __builtin_nontemporal_load(wpanel + (int64_t)min(a0 + i, na - 1) * 64);
+        // every lane loads (lanes past the needed bytes repeat the last
+        // slot): no branch around a load, so the compiler's wait counts stay
+        // exact and the ring below keeps D atoms in flight
+        const int g0 = ac / apg;
+        mt.sr = *reinterpret_cast<const u32x4*>(
+            spanel + min((int64_t)g0 * PW * 2 + 16 * min(lane, SLANES - 1), s_last));
+        mt.zr = *reinterpret_cast<const uint64_t*>(
+            zpanel + min((int64_t)g0 * PW + 8 * min(lane, ZLANES - 1), z_last));
     };
+    // atom j of the run; requests past the run repeat its last atom (a cache
+    // hit, issued without a branch for the same reason)
+    auto load_atom = [&](int j) {
+        return __builtin_nontemporal_load(wrun + (int64_t)min(aw0 + min(j, nw - 1), na - 1) * 64);
+    };
+    u32x4 ring[D];
 
-    auto consume = [&](int r, Buf& b) {
-        const int a0 = a_begin + r * RA + wave * U;
-        if (a0 >= a_end) return;
+    // One round r of the run.
+    auto consume_round = [&](int r, Meta& mt) {
+        const int a0 = aw0 + r * U;
         const int g0 = a0 / apg;
-        int pos = a0 - g0 * apg;      // atom a0's place inside its group
+        int pos = a0 - g0 * apg;      // runtime segments: atom a0's place in its group
         int gl = 0;                   // current group, relative to g0
+
         // stage this wave's x slice and metadata (wave-private LDS)
 #pragma unroll
-        for (int m = 0; m < M; ++m) st.x[m][lane] = b.xr[m];
-        if (16 * lane < Cfg::SB) st.s[lane] = b.sr;
-        if (8 * lane < Cfg::ZB) st.z[lane] = b.zr;
-
-        float alo[M][T], ahi[M][T], sxlo[M], sxhi[M];
-        auto reset = [&]() {
+        for (int m = 0; m < M; ++m) st.x[m][lane] = mt.xr[m];
+        // (lanes past the needed slots rewrite the last slot with its own
+        // value: no branch, which would let the compiler sink the loads into
+        // it and wait for every load in flight)
+        st.s[min(lane, SLANES - 1)] = mt.sr;
+        st.z[min(lane, ZLANES - 1)] = mt.zr;
+        if constexpr (FACT) {
+            // Sums of x per 8-k slice, once for all columns: sx = sum x and
+            // B = sum x * offset (1024 for rows 0,1,4,5 and, 4-bit, 64 for
+            // rows 2,3,6,7).  Lane l holds rows 4(l%2)..+3 of slice l/2: its
+            // first pair has offset 1024, its second 1024 or 64.
+            const half2_t ones = {(_Float16)1.0f, (_Float16)1.0f};
+            const half2_t o_lo = {(_Float16)1024.0f, (_Float16)1024.0f};
+            const half2_t o_hi = BITS == 4 ? half2_t{(_Float16)64.0f, (_Float16)64.0f} : o_lo;
 #pragma unroll
             for (int m = 0; m < M; ++m) {
-                sxlo[m] = 0.f;
-                sxhi[m] = 0.f;
+                const uint32_t x01 = (uint32_t)mt.xr[m], x23 = (uint32_t)(mt.xr[m] >> 32);
+                float sx = __builtin_amdgcn_fdot2(as_h2(x23), ones, __builtin_amdgcn_fdot2(as_h2(x01), ones, 0.f, false), false);
+                float bo = __builtin_amdgcn_fdot2(as_h2(x23), o_hi, __builtin_amdgcn_fdot2(as_h2(x01), o_lo, 0.f, false), false);
+                sx += __shfl_xor(sx, 1);
+                bo += __shfl_xor(bo, 1);
+                // both lanes of a slice store its sums (no branch: a masked
+                // store lets the compiler move the later reads under the mask)
+                st.cs[m][lane] = float2_t{bo, sx};
+            }
+        }
+        // the staged data is read by other lanes of this wave: order the
+        // stores before those reads (a wave-scope fence, no workgroup barrier)
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+        float acc[M][T];                 // factored form: sums of x * code of the open segment
+        float bo[M], sx[M];              // ... and the segment's sums of x * offset and of x
+        half2_t s2[T];                   // dequant form: the open segment's scale and zero-point
+        uint32_t nz[T], nz64[T];
+        auto open = [&]() {
+            if constexpr (FACT) {
+#pragma unroll
+                for (int m = 0; m < M; ++m) {
+                    bo[m] = 0.f;
+                    sx[m] = 0.f;
+#pragma unroll
+                    for (int t = 0; t < T; ++t) acc[m][t] = 0.f;
+                }
+            } else {
+                const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
+                const uint8_t* zp = zbytes + gl * PW + c * T;
 #pragma unroll
                 for (int t = 0; t < T; ++t) {
-                    alo[m][t] = 0.f;
-                    ahi[m][t] = 0.f;
+                    const uint32_t sb = sp[t];
+                    s2[t] = as_h2(sb | (sb << 16));
+                    nz[t] = neg_zero_pair(zp[t]);
+                    if constexpr (BITS == 4) nz64[t] = neg_zero64_pair(nz[t]);
                 }
             }
         };
-        reset();
-        const half2_t ones = {(_Float16)1.0f, (_Float16)1.0f};
-        const uint8_t* sbytes = reinterpret_cast<const uint8_t*>(st.s);
-        const uint8_t* zbytes = reinterpret_cast<const uint8_t*>(st.z);
+        // close the open segment: y += s * (acc - bo - z * sx)
+        auto close = [&]() {
+            if constexpr (FACT) {
+                const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
+                const uint8_t* zp = zbytes + gl * PW + c * T;
+#pragma unroll
+                for (int t = 0; t < T; ++t) {
+                    const float zf = (float)zp[t];
+                    const float sf = (float)__builtin_bit_cast(_Float16, sp[t]);
+#pragma unroll
+                    for (int m = 0; m < M; ++m)
+                        y[m][t] = fmaf(sf, acc[m][t] - fmaf(zf, sx[m], bo[m]), y[m][t]);
+                }
+            }
+        };
 
+        if constexpr (FACT || SEG > 0) open();
 #pragma unroll
         for (int i = 0; i < U; ++i) {
-            const int a = a0 + i;
-            if (a >= a_end) break;
+            const int j = r * U + i;      // atom of the run
+            if (i > 0 && j >= nw) break;
+            // take atom j from the ring and request atom j + D in its place
+            const u32x4 wv = ring[i % D];
+            ring[i % D] = load_atom(j + D);
+            // dequant form, group size known at run time: this atom's metadata
+            if constexpr (!FACT && SEG == 0) open();
             u32x4 xv[M];
 #pragma unroll
             for (int m = 0; m < M; ++m)
                 xv[m] = *reinterpret_cast<const u32x4*>(&st.x[m][(i * kAtomK + 8 * kg) / 4]);
-            const uint32_t wd[4] = {b.w[i][0], b.w[i][1], b.w[i][2], b.w[i][3]};
-            if constexpr (!FACT) {
-                // dequantize once per weight (the GEMM's code: RNE(s (q - z))) and
-                // let every row of A reuse it
-                const uint8_t* zp = zbytes + gl * PW + c * T;
-                const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
-#pragma unroll
-                for (int t = 0; t < T; ++t) {
-                    const uint32_t sb = sp[t];
-                    const half2_t s2 = as_h2(sb | (sb << 16));
-                    half8_t w8;
-                    const uint32_t nz = neg_zero_pair(zp[t]);
-                    if constexpr (BITS == 4)
-                        w8 = dq_w4_dword(wd[t], magic, nz, neg_zero64_pair(nz), s2);
-                    else
-                        w8 = dq_w8_dwords(wd[2 * t], wd[2 * t + 1], nz, s2);
-                    const half2_t w2[4] = {{w8[0], w8[1]}, {w8[2], w8[3]}, {w8[4], w8[5]}, {w8[6], w8[7]}};
-#pragma unroll
-                    for (int m = 0; m < M; ++m) {
-                        float v = y[m][t];
-#pragma unroll
-                        for (int pr = 0; pr < 4; ++pr)
-                            v = __builtin_amdgcn_fdot2(w2[pr], as_h2(xv[m][pr]), v, false);
-                        y[m][t] = v;
-                    }
-                }
-                if (APG > 0 ? (i + 1) % (APG > 0 ? APG : 1) == 0 : ++pos == apg) {
-                    pos = 0;
-                    ++gl;
-                }
-                continue;
-            }
-#pragma unroll
-            for (int t = 0; t < T; ++t) {
-                uint32_t P[4];
-                if constexpr (BITS == 4) {
-                    w4_code_pairs_x16(wd[t], magic, P);
-                } else {
-                    w8_code_pairs(wd[2 * t], P);
-                    w8_code_pairs(wd[2 * t + 1], P + 2);
-                }
-#pragma unroll
-                for (int m = 0; m < M; ++m) {
-                    const uint32_t xd[4] = {xv[m][0], xv[m][1], xv[m][2], xv[m][3]};
-                    float lo = alo[m][t], hi = ahi[m][t];
-                    lo = __builtin_amdgcn_fdot2(as_h2(P[0]), as_h2(xd[0]), lo, false);
-                    lo = __builtin_amdgcn_fdot2(as_h2(P[2]), as_h2(xd[2]), lo, false);
-                    if constexpr (BITS == 4) {
-                        hi = __builtin_amdgcn_fdot2(as_h2(P[1]), as_h2(xd[1]), hi, false);
-                        hi = __builtin_amdgcn_fdot2(as_h2(P[3]), as_h2(xd[3]), hi, false);
-                    } else {
-                        lo = __builtin_amdgcn_fdot2(as_h2(P[1]), as_h2(xd[1]), lo, false);
-                        lo = __builtin_amdgcn_fdot2(as_h2(P[3]), as_h2(xd[3]), lo, false);
-                    }
-                    alo[m][t] = lo;
-                    ahi[m][t] = hi;
-                }
-            }
             if constexpr (FACT) {
 #pragma unroll
                 for (int m = 0; m < M; ++m) {
-                    const uint32_t xd[4] = {xv[m][0], xv[m][1], xv[m][2], xv[m][3]};
-                    float lo = sxlo[m], hi = sxhi[m];
-                    lo = __builtin_amdgcn_fdot2(as_h2(xd[0]), ones, lo, false);
-                    lo = __builtin_amdgcn_fdot2(as_h2(xd[2]), ones, lo, false);
+                    const float2_t v = st.cs[m][8 * i + 2 * kg];   // slice (atom i, kg)
+                    bo[m] += v[0];
+                    sx[m] += v[1];
+                }
+            }
+            const uint32_t wd[4] = {wv[0], wv[1], wv[2], wv[3]};
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                uint32_t P[4];
+                if constexpr (FACT) {
                     if constexpr (BITS == 4) {
-                        hi = __builtin_amdgcn_fdot2(as_h2(xd[1]), ones, hi, false);
-                        hi = __builtin_amdgcn_fdot2(as_h2(xd[3]), ones, hi, false);
+                        w4_code_pairs_sum(wd[t], magic, magic64, P);
                     } else {
-                        lo = __builtin_amdgcn_fdot2(as_h2(xd[1]), ones, lo, false);
-                        lo = __builtin_amdgcn_fdot2(as_h2(xd[3]), ones, lo, false);
+                        w8_code_pairs(wd[2 * t], P);
+                        w8_code_pairs(wd[2 * t + 1], P + 2);
                     }
-                    sxlo[m] = lo;
-                    sxhi[m] = hi;
+                } else {
+                    const half8_t w8 = BITS == 4 ? dq_w4_dword(wd[t], magic, nz[t], nz64[t], s2[t])
+                                                 : dq_w8_dwords(wd[2 * t], wd[2 * t + 1], nz[t], s2[t]);
+                    const u32x4 wu = __builtin_bit_cast(u32x4, w8);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) P[q] = wu[q];
+                }
+#pragma unroll
+                for (int m = 0; m < M; ++m) {
+                    float v = FACT ? acc[m][t] : y[m][t];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) v = __builtin_amdgcn_fdot2(as_h2(P[q]), as_h2(xv[m][q]), v, false);
+                    if constexpr (FACT) acc[m][t] = v; else y[m][t] = v;
                 }
             }
-            // close the group at its last atom or at the end of this wave's run
-            // (with APG known, runs start on group boundaries: see plan_gemv)
-            const bool group_end = APG > 0 ? (i + 1) % (APG > 0 ? APG : 1) == 0 : ++pos == apg;
-            const bool run_end = APG > 0 ? false : (i == U - 1 || a + 1 == a_end);
-            if (group_end || run_end || (APG > 0 && a + 1 == a_end)) {
-                const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
-                const uint8_t* zp = zbytes + gl * PW + c * T;
-#pragma unroll
-                for (int t = 0; t < T; ++t) {
-                    const float s = (float)__builtin_bit_cast(_Float16, sp[t]);
-                    if constexpr (FACT) {
-                        const float zf = (float)zp[t];
-#pragma unroll
-                        for (int m = 0; m < M; ++m) {
-                            float v;
-                            if constexpr (BITS == 4) {
-                                v = fmaf(ahi[m][t], 0.0625f, alo[m][t]);
-                                v = fmaf(-(1024.f + zf), sxlo[m], v);
-                                v = fmaf(-(64.f + zf), sxhi[m], v);
-                            } else {
-                                v = fmaf(-(1024.f + zf), sxlo[m], alo[m][t]);
-                            }
-                            y[m][t] = fmaf(s, v, y[m][t]);
-                        }
-                    }
-                }
-                reset();
+            // end of a segment: end of its group, of the round, or of the run
+            bool seg_end, grp_end;
+            if constexpr (SEG > 0) {
+                grp_end = (i + 1) % SEG == 0;
+                seg_end = grp_end || j + 1 == nw;
+            } else {
+                grp_end = ++pos == apg;
+                seg_end = grp_end || i == U - 1 || j + 1 == nw;
             }
-            if (group_end) {
-                pos = 0;
-                ++gl;
+            if (seg_end) {
+                close();
+                if (i < U - 1) {
+                    if (grp_end) {
+                        ++gl;
+                        pos = 0;
+                    }
+                    if constexpr (FACT || SEG > 0) open();
+                }
             }
         }
     };
 
-    // One round covers K <= 32 * U * WAVES; larger K walks several rounds,
-    // each issuing its loads right before it consumes them.
-    for (int r = 0; r < rounds; ++r) {
-        Buf b;
-        issue(r, b);
-        consume(r, b);
+    if (nrounds > 0) {
+        Meta m0, m1;
+        issue_meta(0, m0);
+#pragma unroll
+        for (int d = 0; d < D; ++d) ring[d] = load_atom(d);
+        // The next round's small loads are issued even past the last round,
+        // at clamped addresses: without a branch around a load the compiler's
+        // wait counts stay exact.  Round 0 is peeled off the loop for the same
+        // reason (waits after a loop header are conservative).
+        issue_meta(1, m1);
+        consume_round(0, m0);
+        for (int r = 1; r < nrounds; r += 2) {
+            issue_meta(r + 1, m0);
+            consume_round(r, m1);
+            if (r + 1 < nrounds) {
+                issue_meta(r + 2, m1);
+                consume_round(r + 1, m0);
+            }
+        }
     }
 
     // Lanes c, c+16, c+32, c+48 hold the same columns: combine over kg.
@@ -323,10 +370,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     // L2 of the XCD from every workgroup.
     float* part = ws_part + (int64_t)p * S * M * PW;
     for (int i = tid; i < M * PW; i += NT) {
-        const int m = i / PW, col = i % PW;
         float v = 0.f;
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) v += sm.red[w][m][col];
+        for (int w = 0; w < WAVES; ++w) v += sm.red[w][i / PW][i % PW];
         __hip_atomic_store(&part[split * M * PW + i], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __builtin_amdgcn_s_waitcnt(0);      // this thread's partial stores have completed
@@ -360,16 +406,22 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 struct GemvPlan {
     int waves, S, AS;
 };
-constexpr int kGemvU = 8, kMaxSplit = 32;
+constexpr int kMaxSplit = 32;
 constexpr int64_t kSplitBelowPanels = 192;      // split K only below this many panels ...
 constexpr int64_t kSplitFromWork = 256;         // ... carrying at least this much work each
 constexpr int64_t kTargetWorkgroups = 256;
 
-inline int gemv_waves(int64_t M) { return M == 1 ? 16 : 8; }
+// 16 waves (four per SIMD) while 128 registers hold a lane's state, else 8.
+constexpr int gemv_waves_for(int M) { return M <= 3 ? 16 : 8; }
+// Weight atoms in flight per wave.  Two measured best on MI355X (graph
+// replay, K=4096 N=14336 and K=14336 N=4096, M = 1..16): four or eight
+// lengthen the memory queues without raising the rate a compute unit streams.
+constexpr int gemv_ring_for(int) { return 2; }
 
 inline GemvPlan plan_gemv(const Layout& L, int64_t M) {
-    const int waves = gemv_waves(M);
-    const int64_t ra = (int64_t)waves * kGemvU;
+    const int waves = gemv_waves_for((int)M);
+    // slices keep at least this many atoms (a round of 16 waves at M = 1, of 8 above)
+    const int64_t ra = (int64_t)(M == 1 ? 16 : 8) * kGemvU;
     const int64_t apg = L.group / kAtomK;
     int64_t S = 1;
     if (L.np < kSplitBelowPanels && L.na * std::max<int64_t>(1, M / 2) >= kSplitFromWork) {
@@ -389,26 +441,27 @@ inline GemvPlan plan_gemv(const Layout& L, int64_t M) {
 // counters where an earlier call (of any shape) left them at zero; then the
 // per-slice partial sums, which are always written before they are read.
 
-
-template <int BITS, int M, int APG>
+template <int BITS, int M, int SEG>
 int launch_g(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, void* ws,
              int mr, hipStream_t s) {
-    constexpr int WAVES = M == 1 ? 16 : 8;
+    constexpr int WAVES = gemv_waves_for(M);
     const GemvPlan sp = plan_gemv(L, M);
     const bool split = ws != nullptr && sp.S > 1;
     uint32_t* cnt = split ? static_cast<uint32_t*>(ws) : nullptr;
     float* part = split ? reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes) : nullptr;
     const int S = split ? sp.S : 1;
     const int AS = split ? sp.AS : (int)L.na;
-    return launch(gemv_kernel<BITS, M, WAVES, kGemvU, APG>, dim3((unsigned)L.np, (unsigned)S),
+    int RW = (AS + WAVES - 1) / WAVES;               // atoms per wave
+    if (SEG > 0) RW = (RW + SEG - 1) / SEG * SEG;    // runs start on group boundaries
+    return launch(gemv_kernel<BITS, M, WAVES, SEG, gemv_ring_for(M)>, dim3((unsigned)L.np, (unsigned)S),
                   dim3(WAVES * 64), 0, s, A, pk, C, (int)L.K, (int)L.N, L.group, L.s_off, L.z_off,
-                  (int)L.na, (int)L.ng, S, AS, part, cnt, mr);
+                  (int)L.na, (int)L.ng, S, AS, RW, part, cnt, mr);
 }
 
 template <int BITS, int M>
 int launch_m(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, void* ws,
              hipStream_t s, int mr = M) {
-    // group 128 (the AWQ default) gets group boundaries fixed at compile time
+    // group 128 (the AWQ default) gets its segments fixed at compile time
     if (L.group == 128) return launch_g<BITS, M, 4>(L, A, pk, C, ws, mr, s);
     return launch_g<BITS, M, 0>(L, A, pk, C, ws, mr, s);
 }

@@ -109,6 +109,7 @@ inline int launch(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t shmem,
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
+typedef float float2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ half2_t as_h2(uint32_t v) { return __builtin_bit_cast(half2_t, v); }
@@ -128,6 +129,14 @@ __device__ __forceinline__ uint32_t magic_reg() {
     return m;
 }
 
+// 0x54005400: fp16 64.0 in both halves.  Its mantissa unit is 1/16, so a
+// nibble placed in bits 4..7 of a half reads as 64 + q, exactly.
+__device__ __forceinline__ uint32_t magic64_reg() {
+    uint32_t m;
+    asm("v_mov_b32 %0, 0x54005400" : "=v"(m));
+    return m;
+}
+
 // Unpack primitives (Section 4.3).  `magic` = kMagic2 (pass magic_reg()).
 // Low nibbles of both halves: (1024 + q, 1024 + q') for the nibbles in bits
 // 0..3 and 16..19 of x.
@@ -138,6 +147,11 @@ __device__ __forceinline__ uint32_t w4_pair_lo(uint32_t x, uint32_t magic) {
 // (1024 + 16 q, 1024 + 16 q'), still exact fp16 integers.
 __device__ __forceinline__ uint32_t w4_pair_hi_x16(uint32_t x, uint32_t magic) {
     return (x & 0x00F000F0u) | magic;
+}
+// Nibbles in bits 4..7 and 20..23 of x as (64 + q, 64 + q') with
+// magic64 = magic64_reg(): exact fp16 integers, no shift.
+__device__ __forceinline__ uint32_t w4_pair_hi_64(uint32_t x, uint32_t magic64) {
+    return (x & 0x00F000F0u) | magic64;
 }
 // Bytes b, b+1 of an 8-bit dword as (1024 + q, 1024 + q'): v_perm_b32 picks
 // bytes of the second operand with selector values 0-3 and of the first
@@ -155,14 +169,16 @@ __device__ __forceinline__ void w4_code_pairs(uint32_t w, uint32_t magic, uint32
     out[3] = w4_pair_lo(w >> 12, magic);
 }
 
-// Cheaper variant for sums: out[0], out[2] are rows (0,1), (4,5) as 1024 + q;
-// out[1], out[3] are rows (2,3), (6,7) as 1024 + 16 q.
-__device__ __forceinline__ void w4_code_pairs_x16(uint32_t w, uint32_t magic, uint32_t out[4]) {
+// Cheaper variant for sums (five instructions per dword): out[0], out[2] are
+// rows (0,1), (4,5) as 1024 + q; out[1], out[3] are rows (2,3), (6,7) as
+// 64 + q.
+__device__ __forceinline__ void w4_code_pairs_sum(uint32_t w, uint32_t magic, uint32_t magic64,
+                                                  uint32_t out[4]) {
     const uint32_t w8 = w >> 8;
     out[0] = w4_pair_lo(w, magic);
-    out[1] = w4_pair_hi_x16(w, magic);
+    out[1] = w4_pair_hi_64(w, magic64);
     out[2] = w4_pair_lo(w8, magic);
-    out[3] = w4_pair_hi_x16(w8, magic);
+    out[3] = w4_pair_hi_64(w8, magic64);
 }
 
 // One 8-bit dword (rows r..r+3, lowest byte first) -> two half2 pairs
@@ -192,7 +208,7 @@ __device__ __forceinline__ uint32_t neg_zero64_pair(uint32_t negz2) {
 // 4-bit, 13 steps:
 //   0      w8 = w >> 8
 //   1..4   unpack: rows (0,1), (4,5) as 1024 + q; rows (2,3), (6,7) read without
-//          a shift as 1024 + 16 q (see w4_code_pairs_x16)
+//          a shift as 1024 + 16 q (see w4_pair_hi_x16)
 //   5, 6   (1024 + q) - (1024 + z) = q - z, exact
 //   7, 8   (1024 + 16 q) / 16 - (64 + z) by one fused multiply-add: its exact
 //          value q - z is an fp16 integer, so its single rounding is exact
