@@ -149,44 +149,52 @@ def sweep(torch, tf, make_inputs, reps=50):
             d = make_inputs(bits, M, K, N, group=GROUP, seed=0, x_std=xstd)
             if bits == 4:
                 p0 = tf.pack_w4(up(d["qweight"]), up(d["qzeros"]), up(d["s"]), K, N, GROUP)
-                fn = tf.w4a16_gemm
             else:
                 p0 = tf.pack_w8(up(d["qweight"]), up(d["zeros"]), up(d["s"]), K, N, GROUP)
-                fn = tf.w8a16_gemm
             ncopy = int(min(40, max(2, -(-(512 << 20) // p0.numel()))))
             copies = [p0] + [p0.clone() for _ in range(ncopy - 1)]
             x = up(d["x"])
             y = torch.empty((M, N), dtype=torch.float16, device=dev)
-            for i in range(5):
-                fn(x, copies[i % ncopy], K, N, GROUP, out=y)
-            torch.cuda.synchronize()
-            # the launches are replayed from a HIP graph, so the host-side cost
-            # of a Python call does not leave the GPU idle between small kernels
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                for i in range(reps):
-                    fn(x, copies[i % ncopy], K, N, GROUP, out=y)
-            g.replay()
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            for _ in range(3):
-                g.replay()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            us = e0.elapsed_time(e1) * 1e3 / (3 * reps)
-            tflops = 2.0 * M * N * K / us / 1e6
-            gbs = algo_bytes(bits, K, N) / us / 1e3
-            hbm_bound = M <= 16
-            print(json.dumps({
-                "workload": name, "bits": bits, "M": M, "K": K, "N": N, "group": GROUP,
-                "us_per_launch": round(us, 3), "TFLOP/s": round(tflops, 2), "GB/s": round(gbs, 1),
-                "bound": "hbm" if hbm_bound else "mfma",
-                "frac": round(gbs / PEAK_HBM_GBS if hbm_bound else tflops / PEAK_F16_TFLOPS, 4),
-                "weight_copies": ncopy, "launches": 3 * reps, "timing": "HIP graph replay"}),
-                flush=True)
-            del g, copies, p0, x, y, d
+            # decode shapes go through both entry points (the GEMV is vector-ALU
+            # only; the GEMM entry may use the matrix cores from 4 rows up)
+            for entry in (("gemv", "gemm") if M <= tf.GEMV_MAX_M else ("gemm",)):
+                sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps)
+            del copies, p0, x, y, d
             torch.cuda.empty_cache()
+
+
+def sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps):
+    fn = getattr(tf, f"w{bits}a16_{entry}")
+    ncopy = len(copies)
+    for i in range(5):
+        fn(x, copies[i % ncopy], K, N, GROUP, out=y)
+    torch.cuda.synchronize()
+    # the launches are replayed from a HIP graph, so the host-side cost
+    # of a Python call does not leave the GPU idle between small kernels
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(reps):
+            fn(x, copies[i % ncopy], K, N, GROUP, out=y)
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(3):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (3 * reps)
+    tflops = 2.0 * M * N * K / us / 1e6
+    gbs = algo_bytes(bits, K, N) / us / 1e3
+    hbm_bound = M <= 16
+    print(json.dumps({
+        "workload": name, "entry": entry, "bits": bits, "M": M, "K": K, "N": N, "group": GROUP,
+        "us_per_launch": round(us, 3), "TFLOP/s": round(tflops, 2), "GB/s": round(gbs, 1),
+        "bound": "hbm" if hbm_bound else "mfma",
+        "frac": round(gbs / PEAK_HBM_GBS if hbm_bound else tflops / PEAK_F16_TFLOPS, 4),
+        "weight_copies": ncopy, "launches": 3 * reps, "timing": "HIP graph replay"}),
+        flush=True)
+    del g
 
 
 def main():

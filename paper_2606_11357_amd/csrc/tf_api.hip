@@ -17,9 +17,14 @@ int check_weight(int bits, int64_t K, int64_t N, int group) {
     return TF_OK;
 }
 
-// Bytes of workspace the matmul kernels of this problem can use.
+// Bytes of workspace the matmul kernels of this problem can use (the GEMM
+// and GEMV entry points may pick different kernels for the same M: the
+// larger need of the two).
 int64_t workspace_bytes(const Layout& L, int64_t M) {
-    return M <= tf::kSkinnyMaxM ? tf::gemv_workspace_bytes(L, M) : tf::gemm_workspace_bytes(L, M);
+    if (M > tf::kSkinnyMaxM) return tf::gemm_workspace_bytes(L, M);
+    const int64_t gemv = tf::gemv_workspace_bytes(L, M);
+    const int64_t skinny = M >= tf::kSkinnyMinM ? tf::skinny_workspace_bytes(L) : 0;
+    return gemv > skinny ? gemv : skinny;
 }
 
 int check_matmul(int bits, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
@@ -49,7 +54,8 @@ int gemm_entry(int bits, const uint16_t* A, const void* packed, uint16_t* C, int
     rc = check_workspace(L, M, ws, ws_bytes);
     if (rc) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (M <= tf::kSkinnyMaxM) return tf::launch_gemv(L, A, packed, C, M, ws, s);
+    if (M < tf::kSkinnyMinM) return tf::launch_gemv(L, A, packed, C, M, ws, s);
+    if (M <= tf::kSkinnyMaxM) return tf::launch_skinny_gemm(L, A, packed, C, M, ws, s);
     return tf::launch_gemm(L, A, packed, C, M, ws, ws_bytes, s);
 }
 

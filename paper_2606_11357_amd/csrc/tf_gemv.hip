@@ -1,10 +1,11 @@
 // Decode GEMV (Section 2.1: batch-1 generation makes linear layers
 // matrix-vector products; Section 4.3 "GEMV microkernel"; Section 4.4).
 //
-// y[m, n] = sum_k x[m, k] * s[g, n] * (q[k, n] - z[g, n]),  1 <= M <= 8; the
-// same kernel with 16 row slots also serves the GEMM entry points for
-// 9 <= M <= 16 (skinny prefill), where the weights, not the matrix cores,
-// bound the time.
+// y[m, n] = sum_k x[m, k] * s[g, n] * (q[k, n] - z[g, n]),  1 <= M <= 8, on
+// the vector ALU only.  The same streaming kernel with 16 row slots serves
+// the GEMM entry points for few rows (skinny prefill, 4 <= M <= 16): there
+// each dequantized dword is the B operand of one v_mfma_f32_16x16x32_f16 and
+// the weights, not the matrix cores, bound the time.
 //
 // Mapping (the GPU form of the principle of Section 4.4: every compute unit
 // streams its own weight slice, the activations are shared, each workgroup
@@ -53,13 +54,17 @@ struct GemvCfg {
     static constexpr int T = BITS == 4 ? 4 : 2;      // columns per lane
     static constexpr int PW = BITS == 4 ? 64 : 32;   // panel width
     static constexpr bool FACT = M <= kFactMaxM;
+    // 16 row slots (GEMM calls with few rows): matrix cores, A read per atom
+    static constexpr bool MF = M > TF_GEMV_MAX_M;
+    static constexpr int XR = MF ? 1 : M;             // rows of x staged in LDS
+    static constexpr int CR = FACT ? M : 1;           // rows of slice sums
 };
 
 // One wave's staging area in LDS (private to the wave: no barrier needed).
-template <int M, int PW>
+template <int XR, int CR, int PW>
 struct WaveStage {
-    uint64_t x[M][64];                  // lane l holds k = 4l..4l+3 of the round's 256
-    float2_t cs[M][64];                 // factored form: lane l: sums of 8-k slice l / 2
+    uint64_t x[XR][64];                 // lane l holds k = 4l..4l+3 of the round's 256
+    float2_t cs[CR][64];                // factored form: lane l: sums of 8-k slice l / 2
     u32x4 s[kGemvU * PW * 2 / 16];      // scales of up to U groups
     uint64_t z[kGemvU * PW / 8];        // zero-points of up to U groups
 };
@@ -76,14 +81,15 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     // (in bounds) and are never stored.
     using Cfg = GemvCfg<BITS, M>;
     constexpr int U = kGemvU, T = Cfg::T, PW = Cfg::PW;
-    constexpr bool FACT = Cfg::FACT;
+    constexpr bool FACT = Cfg::FACT, MF = Cfg::MF;
     constexpr int NT = WAVES * 64;
+    static_assert(!MF || M == 16, "the matrix-core form holds exactly 16 rows");
     static_assert(SEG == 0 || U % SEG == 0, "segments tile a round");
     static_assert(U % D == 0, "the load ring tiles a round");
     // metadata of the groups one round touches: U / SEG groups, or up to U
     constexpr int NGR = SEG > 0 ? U / SEG : U;
     constexpr int SLANES = NGR * PW * 2 / 16, ZLANES = NGR * PW / 8;
-    using Stage = WaveStage<M, PW>;
+    using Stage = WaveStage<Cfg::XR, Cfg::CR, PW>;
     union Smem {
         Stage st[WAVES];
         float red[WAVES][M][PW];
@@ -128,17 +134,19 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     // lets the first-needed bytes arrive anywhere in the whole transfer).
     // Addresses are clamped into the panel, so every load is in bounds.
     struct Meta {
-        uint64_t xr[M];
+        uint64_t xr[Cfg::XR];
         u32x4 sr;
         uint64_t zr;
     };
     auto issue_meta = [&](int r, Meta& mt) {
         const int ac = min(aw0 + r * U, na - 1);
         const int k0 = ac * kAtomK;
+        if constexpr (!MF) {
 #pragma unroll
-        for (int m = 0; m < M; ++m) {
-            const int k = min(k0 + 4 * lane, K - 4);
-            mt.xr[m] = *reinterpret_cast<const uint64_t*>(A + (int64_t)min(m, mr - 1) * K + k);
+            for (int m = 0; m < M; ++m) {
+                const int k = min(k0 + 4 * lane, K - 4);
+                mt.xr[m] = *reinterpret_cast<const uint64_t*>(A + (int64_t)min(m, mr - 1) * K + k);
+            }
         }
         // every lane loads (lanes past the needed bytes repeat the last
         // slot): no branch around a load, so the compiler's wait counts stay
@@ -155,6 +163,18 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         return __builtin_nontemporal_load(wrun + (int64_t)min(aw0 + min(j, nw - 1), na - 1) * 64);
     };
     u32x4 ring[D];
+    // Matrix-core form: the A operand of v_mfma_f32_16x16x32_f16 for atom j,
+    // row c (row slots past mr repeat row mr - 1), k = 32 a + 8 kg + 0..7,
+    // read straight from global memory (A is small and stays in L2) through
+    // a ring of its own.
+    const uint16_t* arow = A + (int64_t)min(c, mr - 1) * K + 8 * kg;
+    auto load_afrag = [&](int j) {
+        return *reinterpret_cast<const u32x4*>(arow + (int64_t)min(aw0 + min(j, nw - 1), na - 1) * kAtomK);
+    };
+    u32x4 aring[MF ? D : 1];
+    float4_t macc[MF ? T : 1];          // lane (c, kg): rows 4 kg + 0..3, columns c + 16 t
+#pragma unroll
+    for (int t = 0; t < (MF ? T : 1); ++t) macc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
 
     // One round r of the run.
     auto consume_round = [&](int r, Meta& mt) {
@@ -164,8 +184,10 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         int gl = 0;                   // current group, relative to g0
 
         // stage this wave's x slice and metadata (wave-private LDS)
+        if constexpr (!MF) {
 #pragma unroll
-        for (int m = 0; m < M; ++m) st.x[m][lane] = mt.xr[m];
+            for (int m = 0; m < M; ++m) st.x[m][lane] = mt.xr[m];
+        }
         // (lanes past the needed slots rewrite the last slot with its own
         // value: no branch, which would let the compiler sink the loads into
         // it and wait for every load in flight)
@@ -246,12 +268,19 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
             // take atom j from the ring and request atom j + D in its place
             const u32x4 wv = ring[i % D];
             ring[i % D] = load_atom(j + D);
+            u32x4 afrag;
+            if constexpr (MF) {
+                afrag = aring[i % D];
+                aring[i % D] = load_afrag(j + D);
+            }
             // dequant form, group size known at run time: this atom's metadata
             if constexpr (!FACT && SEG == 0) open();
-            u32x4 xv[M];
+            u32x4 xv[Cfg::XR];
+            if constexpr (!MF) {
 #pragma unroll
-            for (int m = 0; m < M; ++m)
-                xv[m] = *reinterpret_cast<const u32x4*>(&st.x[m][(i * kAtomK + 8 * kg) / 4]);
+                for (int m = 0; m < M; ++m)
+                    xv[m] = *reinterpret_cast<const u32x4*>(&st.x[m][(i * kAtomK + 8 * kg) / 4]);
+            }
             if constexpr (FACT) {
 #pragma unroll
                 for (int m = 0; m < M; ++m) {
@@ -274,6 +303,12 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                 } else {
                     const half8_t w8 = BITS == 4 ? dq_w4_dword(wd[t], magic, nz[t], nz64[t], s2[t])
                                                  : dq_w8_dwords(wd[2 * t], wd[2 * t + 1], nz[t], s2[t]);
+                    if constexpr (MF) {
+                        // the dequantized dword is the B operand of columns c + 16 t
+                        macc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                            __builtin_bit_cast(half8_t, afrag), w8, macc[t], 0, 0, 0);
+                        continue;
+                    }
                     const u32x4 wu = __builtin_bit_cast(u32x4, w8);
 #pragma unroll
                     for (int q = 0; q < 4; ++q) P[q] = wu[q];
@@ -312,7 +347,10 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         Meta m0, m1;
         issue_meta(0, m0);
 #pragma unroll
-        for (int d = 0; d < D; ++d) ring[d] = load_atom(d);
+        for (int d = 0; d < D; ++d) {
+            ring[d] = load_atom(d);
+            if constexpr (MF) aring[d] = load_afrag(d);
+        }
         // The next round's small loads are issued even past the last round,
         // at clamped addresses: without a branch around a load the compiler's
         // wait counts stay exact.  Round 0 is peeled off the loop for the same
@@ -329,22 +367,31 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         }
     }
 
-    // Lanes c, c+16, c+32, c+48 hold the same columns: combine over kg.
+    if constexpr (MF) {
+        // each lane holds distinct outputs: rows 4 kg + 0..3 of columns c + 16 t
+        __syncthreads();   // staging storage becomes the reduction buffer
 #pragma unroll
-    for (int m = 0; m < M; ++m)
+        for (int t = 0; t < T; ++t)
 #pragma unroll
-        for (int t = 0; t < T; ++t) {
-            float v = y[m][t];
-            v += __shfl_xor(v, 16);
-            v += __shfl_xor(v, 32);
-            y[m][t] = v;
-        }
-    __syncthreads();   // staging storage becomes the reduction buffer
-    if (kg == 0) {
+            for (int q = 0; q < 4; ++q) sm.red[wave][4 * kg + q][c + 16 * t] = macc[t][q];
+    } else {
+        // Lanes c, c+16, c+32, c+48 hold the same columns: combine over kg.
 #pragma unroll
         for (int m = 0; m < M; ++m)
 #pragma unroll
-            for (int t = 0; t < T; ++t) sm.red[wave][m][c + 16 * t] = y[m][t];
+            for (int t = 0; t < T; ++t) {
+                float v = y[m][t];
+                v += __shfl_xor(v, 16);
+                v += __shfl_xor(v, 32);
+                y[m][t] = v;
+            }
+        __syncthreads();   // staging storage becomes the reduction buffer
+        if (kg == 0) {
+#pragma unroll
+            for (int m = 0; m < M; ++m)
+#pragma unroll
+                for (int t = 0; t < T; ++t) sm.red[wave][m][c + 16 * t] = y[m][t];
+        }
     }
     __syncthreads();
     if (S == 1) {
@@ -410,6 +457,7 @@ constexpr int kMaxSplit = 32;
 constexpr int64_t kSplitBelowPanels = 192;      // split K only below this many panels ...
 constexpr int64_t kSplitFromWork = 256;         // ... carrying at least this much work each
 constexpr int64_t kTargetWorkgroups = 256;
+constexpr int64_t kMfSliceAtoms = 64;
 
 // 16 waves (four per SIMD) while 128 registers hold a lane's state, else 8.
 constexpr int gemv_waves_for(int M) { return M <= 3 ? 16 : 8; }
@@ -420,8 +468,10 @@ constexpr int gemv_ring_for(int) { return 2; }
 
 inline GemvPlan plan_gemv(const Layout& L, int64_t M) {
     const int waves = gemv_waves_for((int)M);
-    // slices keep at least this many atoms (a round of 16 waves at M = 1, of 8 above)
-    const int64_t ra = (int64_t)(M == 1 ? 16 : 8) * kGemvU;
+    // slices keep at least this many atoms: a round of 16 waves at M = 1, of
+    // 8 up to 8 rows; the matrix-core form (little vector work per atom)
+    // splits down to kMfSliceAtoms
+    const int64_t ra = M > TF_GEMV_MAX_M ? kMfSliceAtoms : (int64_t)(M == 1 ? 16 : 8) * kGemvU;
     const int64_t apg = L.group / kAtomK;
     int64_t S = 1;
     if (L.np < kSplitBelowPanels && L.na * std::max<int64_t>(1, M / 2) >= kSplitFromWork) {
@@ -480,24 +530,35 @@ int launch_bits(const Layout& L, const uint16_t* A, const void* packed, uint16_t
         case 7: return launch_m<BITS, 7>(L, A, pk, C, ws, s);
         case 8: return launch_m<BITS, 8>(L, A, pk, C, ws, s);
     }
-    if (M <= kSkinnyMaxM) return launch_m<BITS, kSkinnyMaxM>(L, A, pk, C, ws, s, (int)M);
     return TF_ERR_ARG;
 }
 
-}  // namespace
-
-int64_t gemv_workspace_bytes(const Layout& L, int64_t M) {
-    if (M < 1 || M > kSkinnyMaxM) return 0;
-    const int64_t slots = M <= TF_GEMV_MAX_M ? M : kSkinnyMaxM;    // row slots of the kernel
+int64_t workspace_for_slots(const Layout& L, int64_t slots) {
     const GemvPlan sp = plan_gemv(L, slots);
     if (sp.S <= 1) return 0;
     return kWsCounterBytes + align256((int64_t)L.np * sp.S * slots * L.pw * 4);
 }
 
+}  // namespace
+
+int64_t gemv_workspace_bytes(const Layout& L, int64_t M) {
+    return M >= 1 && M <= TF_GEMV_MAX_M ? workspace_for_slots(L, M) : 0;
+}
+
+int64_t skinny_workspace_bytes(const Layout& L) { return workspace_for_slots(L, kSkinnyMaxM); }
+
 int launch_gemv(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, hipStream_t s) {
     return L.bits == 4 ? launch_bits<4>(L, A, packed, C, M, ws, s)
                        : launch_bits<8>(L, A, packed, C, M, ws, s);
+}
+
+int launch_skinny_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C,
+                       int64_t M, void* ws, hipStream_t s) {
+    if (M < 1 || M > kSkinnyMaxM) return TF_ERR_ARG;
+    const uint8_t* pk = static_cast<const uint8_t*>(packed);
+    return L.bits == 4 ? launch_m<4, kSkinnyMaxM>(L, A, pk, C, ws, s, (int)M)
+                       : launch_m<8, kSkinnyMaxM>(L, A, pk, C, ws, s, (int)M);
 }
 
 }  // namespace tf

@@ -48,7 +48,9 @@ constexpr int kLayoutVersion = 1;
 constexpr int64_t kWsCounterBytes = (TF_MAX_DIM / 32) * 4;
 // Most workgroups a stream-K GEMM launch uses (sizes its workspace).
 constexpr int kSkMaxGroups = 256;
-// GEMM calls with up to this many rows run the GEMV kernel (16 row slots).
+// GEMM calls with kSkinnyMinM..kSkinnyMaxM rows run the streaming kernel's
+// matrix-core form (16 row slots); fewer rows run the decode GEMV.
+constexpr int kSkinnyMinM = 4;
 constexpr int kSkinnyMaxM = 16;
 constexpr int kAtomK = 32;
 constexpr int kAtomBytes = 1024;
@@ -292,8 +294,11 @@ int launch_unpack(const Layout& L, const void* packed, uint8_t* q_out, uint8_t* 
 int launch_dequant(const Layout& L, const void* packed, int out_dtype, void* w_out,
                    hipStream_t s);
 int64_t gemv_workspace_bytes(const Layout& L, int64_t M);
+int64_t skinny_workspace_bytes(const Layout& L);
 int launch_gemv(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, hipStream_t s);
+int launch_skinny_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C,
+                       int64_t M, void* ws, hipStream_t s);
 int64_t gemm_workspace_bytes(const Layout& L, int64_t M);
 bool gemm256_supported(const Layout& L);
 bool gemm256_fills_device(const Layout& L, int64_t M);

@@ -162,7 +162,10 @@ GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 2
                (4, 600, 1024, 1040, 128), (8, 520, 512, 776, 64), (4, 513, 256, 2056, 32),
                (4, 1100, 512, 1040, 128), (8, 1030, 512, 776, 64), (4, 1280, 256, 520, 32),
                (8, 1025, 1024, 264, 1024), (4, 1024, 640, 2048, 64),
-               (4, 12, 1024, 200, 64), (8, 16, 2048, 264, 128), (4, 13, 512, 1032, 32), (8, 10, 384, 40, 128)]
+               (4, 12, 1024, 200, 64), (8, 16, 2048, 264, 128), (4, 13, 512, 1032, 32), (8, 10, 384, 40, 128),
+               # 4..8 rows through the GEMM entry: the matrix-core streaming form
+               (4, 4, 512, 136, 128), (8, 5, 384, 40, 32), (4, 8, 1024, 200, 64), (8, 7, 2048, 264, 128),
+               (4, 6, 288, 72, 96), (4, 3, 256, 64, 128)]
 
 
 @pytest.mark.parametrize("bits,M,K,N,G", GEMM_SHAPES)
@@ -174,7 +177,8 @@ def test_gemm_parity_small(tf, bits, M, K, N, G):
 @pytest.mark.parametrize("kind,bits,M,K,N", [("gemv", 4, 8, 4096, 1024), ("gemv", 8, 8, 4096, 512),
                                              ("gemm", 8, 256, 4096, 512), ("gemm", 4, 200, 8192, 256),
                                              ("gemv", 4, 1, 32768, 64), ("gemm", 4, 1030, 8192, 512),
-                                             ("gemm", 8, 1024, 4096, 768)])
+                                             ("gemm", 8, 1024, 4096, 768), ("gemm", 4, 16, 4096, 1024),
+                                             ("gemm", 8, 5, 8192, 512)])
 def test_integer_invariant_bitexact(tf, kind, bits, M, K, N):
     """s = 1, z = 0, integer x in [-3, 3]: every partial sum is an integer below
     2^24, so the fp16 output must be RNE of the exact integer matmul."""
