@@ -136,9 +136,9 @@ int64_t tf_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group)
 /*
  * Prefill GEMM (Section 2.1: M grows with the prompt length):
  *   C_f16[M, N] = A_f16[M, K] x dequant(packed)[K, N], fp32 accumulate, RNE.
- * Any M >= 1.  M <= 3 runs the decode GEMV; 4 <= M <= 16 a weight-streaming
- * kernel that feeds each dequantized dword to one matrix-core instruction
- * (16 row slots); larger M the tiled matrix-core GEMMs.  The dequantized
+ * Any M >= 1.  M <= 3 runs the decode GEMV; 4 <= M <= 64 a weight-streaming
+ * kernel that feeds each dequantized dword to matrix-core instructions (16,
+ * 32 or 64 row slots); larger M the tiled matrix-core GEMMs.  The dequantized
  * fp16 weight fed to the matrix cores is RNE(s * (q - z)), rounded once.
  * workspace: see tf_workspace_bytes.
  */

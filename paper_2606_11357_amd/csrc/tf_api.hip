@@ -23,7 +23,7 @@ int check_weight(int bits, int64_t K, int64_t N, int group) {
 int64_t workspace_bytes(const Layout& L, int64_t M) {
     if (M > tf::kSkinnyMaxM) return tf::gemm_workspace_bytes(L, M);
     const int64_t gemv = tf::gemv_workspace_bytes(L, M);
-    const int64_t skinny = M >= tf::kSkinnyMinM ? tf::skinny_workspace_bytes(L) : 0;
+    const int64_t skinny = M >= tf::kSkinnyMinM ? tf::skinny_workspace_bytes(L, M) : 0;
     return gemv > skinny ? gemv : skinny;
 }
 

@@ -19,7 +19,14 @@
 //  - Tiles are numbered so that each XCD (workgroups are dealt round-robin
 //    over the 8 XCDs) works on a contiguous band of tiles sharing rows of A,
 //    which then stay in that XCD's L2.
+//  - When the tiles are too few to occupy the device and a workspace is
+//    given, each tile's K is cut into S slices of whole chunks, one workgroup
+//    each; a slice parks its fp32 partial tile in the workspace and the last
+//    slice of a tile to arrive adds all of them in slice order (bitwise
+//    reproducible) and writes C.
 #include "tf_internal.h"
+
+#include <algorithm>
 
 namespace tf {
 namespace {
@@ -40,11 +47,19 @@ __device__ __forceinline__ int a_slot(int row, int ch) { return row * 4 + (ch ^ 
 
 // MPC: metadata groups per chunk (1 when a group spans the whole chunk, else
 // chunk rows / group); the group of step j is j / (chunk steps / MPC).
+// Split-K arguments: S slices per tile of cps chunks each (S = 1: no split);
+// arrival counters (zero at rest) and partial tiles in the workspace.
+struct SplitK {
+    int S, cps;
+    uint32_t* cnt;
+    float* part;
+};
+
 template <int BITS, int MPC>
 __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
     int M, int K, int N, int gshift, int64_t s_off, int64_t z_off, int na, int ng, int np,
-    int tiles_m, int tiles_n) {
+    int tiles_m, int tiles_n, SplitK sk) {
     constexpr int PW = BITS == 4 ? 64 : 32;
     constexpr int T = PW / 16;                 // columns per lane per atom
     constexpr int PANELS = 64 / PW;            // panels per wave
@@ -57,17 +72,23 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
     const int c = lane & 15, kg = lane >> 4;
     const uint32_t magic = magic_reg();
 
-    // XCD-aware tile order: block b runs on XCD b % 8; XCD x takes the x-th
-    // contiguous band of the row-major tile list.
-    const int total = tiles_m * tiles_n;
-    int tile;
+    // XCD-aware order: block b runs on XCD b % 8; XCD x takes the x-th
+    // contiguous band of the row-major list of (tile, slice) units, so the
+    // slices of a tile and neighbouring tiles share that XCD's L2.
+    const int total = tiles_m * tiles_n * sk.S;
+    int unit;
     {
         const int b = blockIdx.x;
         const int per = total / kXcds, rem = total % kXcds;
         const int x = b % kXcds, i = b / kXcds;
-        tile = x * per + min(x, rem) + i;
+        unit = x * per + min(x, rem) + i;
     }
+    const int tile = unit / sk.S, split = unit % sk.S;
     const int tm = tile / tiles_n, tn = tile % tiles_n;
+    constexpr int CS0 = chunk_steps<BITS>();
+    const int ch0 = split * sk.cps;                            // first chunk of this slice
+    const int chunks = min(na / CS0 - ch0, sk.cps);            // chunks of this slice (>= 1)
+    const int st0 = ch0 * CS0;                                 // first step of this slice
     const int64_t row0 = (int64_t)tm * kBM;
     const int64_t col0 = (int64_t)tn * kBN + wave * 64;      // this wave's 64 columns
 
@@ -85,10 +106,10 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
     for (int r = 0; r < 2; ++r) {
         const int idx = tid + kGemmThreads * r;
         const int64_t grow = min<int64_t>(row0 + (idx >> 2), (int64_t)M - 1);
-        arow[r] = A + grow * K + (idx & 3) * 8;
+        arow[r] = A + grow * K + (idx & 3) * 8 + (int64_t)st0 * kBK;
         aslot[r] = a_slot(idx >> 2, idx & 3);
     }
-    const int steps = na;                      // one 32-row step per atom
+    const int steps = chunks * CS0;            // one 32-row step per atom
     auto load_a = [&](int step, u32x4 (&av)[2]) {
         step = min(step, steps - 1);           // clamped: a repeated valid step, never used
 #pragma unroll
@@ -110,7 +131,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
         int64_t panel = col0 / PW + pp;
         live = live || panel < np;
         panel = min<int64_t>(panel, np - 1);
-        wp[pp] = reinterpret_cast<const u32x4*>(packed) + panel * na * 64 + lane;
+        wp[pp] = reinterpret_cast<const u32x4*>(packed) + (panel * na + st0) * 64 + lane;
         sp[pp] = packed + s_off + (panel * ng * PW + c * T) * 2;
         zp[pp] = packed + z_off + panel * ng * PW + c * T;
     }
@@ -118,8 +139,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
     // in slot s % kChunkSteps, is loaded three steps ahead and is dequantized
     // one step ahead, while the MFMAs of the step before it run.  Raw metadata
     // is loaded a chunk ahead; group constants are formed once per group.
-    constexpr int CS = kChunkSteps;
-    const int chunks = steps / CS;            // the launcher requires K % (32 * CS) == 0
+    constexpr int CS = kChunkSteps;           // the launcher requires K % (32 * CS) == 0
     u32x4 ring[CS][PANELS];
     auto load_atom = [&](int step, u32x4 (&slot)[PANELS]) {
         step = min(step, steps - 1);           // clamped: a repeated valid step, never used
@@ -134,7 +154,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
         ch = min(ch, chunks - 1);
 #pragma unroll
         for (int m = 0; m < MPC; ++m) {
-            const int g = ((ch * CS + m * SPG) * kAtomK) >> gshift;
+            const int g = (((ch0 + ch) * CS + m * SPG) * kAtomK) >> gshift;
 #pragma unroll
             for (int pp = 0; pp < PANELS; ++pp) {
                 if constexpr (BITS == 4) {
@@ -231,18 +251,63 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
     }
 
     // ---- epilogue: lane holds column c of each 16x16 block, rows 4 kg + r
+    auto store = [&](auto&& total_of) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const int64_t col = col0 + 16 * t + c;
+            for (int t = 0; t < 4; ++t) {
+                const float4_t v = total_of(i, t);
+                const int64_t col = col0 + 16 * t + c;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t row = row0 + 16 * i + 4 * kg + r;
-                if (row < M && col < N)
-                    C[row * N + col] = __builtin_bit_cast(uint16_t, (_Float16)acc[i][t][r]);
+                for (int r = 0; r < 4; ++r) {
+                    const int64_t row = row0 + 16 * i + 4 * kg + r;
+                    if (row < M && col < N) C[row * N + col] = __builtin_bit_cast(uint16_t, (_Float16)v[r]);
+                }
             }
+    };
+    if (sk.S == 1) {
+        store([&](int i, int t) { return acc[i][t]; });
+        return;
+    }
+    // Park this slice's partial tile (wave w's 128 x 64 part, block (i, t) as
+    // 64 consecutive float4, one per lane) with device-coherent stores; wait
+    // for them to complete before counting the arrival.
+    constexpr uint32_t kWavePart = kBM * 64 * 4;              // bytes of a wave's part
+    auto part_rsrc = [&](int sl) {
+        return make_rsrc(sk.part + ((int64_t)tile * sk.S + sl) * (kBM * kBN) + wave * (kBM * 64), kWavePart);
+    };
+    {
+        const __amdgpu_buffer_rsrc_t pr = part_rsrc(split);
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, acc[i][t]), pr,
+                                                       (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, kSc1);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    __shared__ int last;
+    if (tid == 0)
+        last = __hip_atomic_fetch_add(&sk.cnt[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+               (uint32_t)(sk.S - 1);
+    __syncthreads();
+    if (!last) return;
+    // The last slice adds the tile's slices in order: those before it, its
+    // own from registers, those after it.
+    store([&](int i, int t) {
+        const uint32_t off = (uint32_t)(((i * 4 + t) * 64 + lane) * 16);
+        float4_t r = {0.f, 0.f, 0.f, 0.f};
+        for (int sl = 0; sl < sk.S; ++sl) {
+            if (sl == split)
+                r += acc[i][t];
+            else
+                r += __builtin_bit_cast(float4_t, __builtin_amdgcn_raw_buffer_load_b128(part_rsrc(sl), off, 0, kSc1));
         }
+        return r;
+    });
+    if (tid == 0)   // leave the counter at zero for the next call
+        __hip_atomic_store(&sk.cnt[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Generic kernel for the cases the main one leaves out (K not a multiple of
@@ -349,28 +414,73 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_generic(
         }
 }
 
+// Split plan of the main kernel: K is cut only when a workspace is given and
+// the tiles are fewer than kSplitBelowTiles; slices keep at least
+// kMinSliceChunks chunks.  Aiming at about 128 units (rather than one per
+// compute unit) measured fastest on MI355X: the slice that finishes a tile
+// reads the others' partial tiles alone, at one compute unit's rate.
+struct SplitPlan {
+    int S, cps;
+};
+constexpr int kSplitBelowTiles = 256;
+constexpr int kTargetUnits = 128;
+constexpr int kMinSliceChunks = 4;
+
+template <int BITS>
+SplitPlan plan_split(const Layout& L, int64_t M) {
+    const int64_t tiles = ((M + kBM - 1) / kBM) * ((L.N + kBN - 1) / kBN);
+    const int chunks = (int)(L.K / (kBK * chunk_steps<BITS>()));
+    int S = 1;
+    if (tiles < kSplitBelowTiles) {
+        S = (int)std::min<int64_t>((kTargetUnits + tiles - 1) / tiles, chunks / kMinSliceChunks);
+        S = std::max(S, 1);
+    }
+    const int cps = (chunks + S - 1) / S;
+    return {(chunks + cps - 1) / cps, cps};    // no empty slice
+}
+
+// Workspace of a split plan: arrival counters (one per tile, fixed region),
+// then one fp32 partial tile per (tile, slice).
+int64_t split_workspace_bytes(const Layout& L, int64_t M, const SplitPlan& sp) {
+    if (sp.S <= 1) return 0;
+    const int64_t tiles = ((M + kBM - 1) / kBM) * ((L.N + kBN - 1) / kBN);
+    return kWsCounterBytes + tiles * sp.S * (int64_t)(kBM * kBN * 4);
+}
+
+bool main_kernel_fits(const Layout& L, int bits) {
+    const int chunk_rows = kBK * 4;
+    return L.K % chunk_rows == 0 && (L.group & (L.group - 1)) == 0 && bits > 0;
+}
+
 template <int BITS, int MPC>
 int launch_main(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
-                hipStream_t s) {
+                void* ws, hipStream_t s) {
     const int tiles_m = (int)((M + kBM - 1) / kBM);
     const int tiles_n = (int)((L.N + kBN - 1) / kBN);
     const int gshift = __builtin_ctz((unsigned)L.group);
-    return launch(gemm_kernel<BITS, MPC>, dim3((unsigned)(tiles_m * tiles_n)), dim3(kGemmThreads), 0, s,
-                  A, pk, C, (int)M, (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na,
-                  (int)L.ng, (int)L.np, tiles_m, tiles_n);
+    SplitPlan sp = plan_split<BITS>(L, M);
+    if (!ws) sp = {1, (int)(L.K / (kBK * chunk_steps<BITS>()))};
+    SplitK sk{sp.S, sp.cps, nullptr, nullptr};
+    if (sp.S > 1) {
+        sk.cnt = static_cast<uint32_t*>(ws);
+        sk.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes);
+    }
+    return launch(gemm_kernel<BITS, MPC>, dim3((unsigned)(tiles_m * tiles_n * sp.S)), dim3(kGemmThreads),
+                  0, s, A, pk, C, (int)M, (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na,
+                  (int)L.ng, (int)L.np, tiles_m, tiles_n, sk);
 }
 
 template <int BITS>
 int launch_bits(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
-                hipStream_t s) {
+                void* ws, hipStream_t s) {
     constexpr int CS = chunk_steps<BITS>();
     const int chunk_rows = kBK * CS;
     const bool pow2_group = (L.group & (L.group - 1)) == 0;
     if (L.K % chunk_rows == 0 && pow2_group) {
         const int mpc = L.group >= chunk_rows ? 1 : chunk_rows / L.group;
-        if (mpc == 1) return launch_main<BITS, 1>(L, A, pk, C, M, s);
-        if (mpc == 2) return launch_main<BITS, 2>(L, A, pk, C, M, s);
-        if constexpr (CS >= 4) return launch_main<BITS, 4>(L, A, pk, C, M, s);
+        if (mpc == 1) return launch_main<BITS, 1>(L, A, pk, C, M, ws, s);
+        if (mpc == 2) return launch_main<BITS, 2>(L, A, pk, C, M, ws, s);
+        if constexpr (CS >= 4) return launch_main<BITS, 4>(L, A, pk, C, M, ws, s);
     }
     dim3 grid((unsigned)((L.N + kBN1 - 1) / kBN1), (unsigned)((M + kBM1 - 1) / kBM1));
     return launch(gemm_kernel_generic<BITS>, grid, dim3(kGemmThreads), 0, s, A, pk, C, (int)M,
@@ -387,15 +497,23 @@ static bool use_gemm256(const Layout& L, int64_t M, const void* ws) {
     return M >= kGemm256MinM && gemm256_supported(L) && (ws != nullptr || gemm256_fills_device(L, M));
 }
 
+// Workspace either GEMM may use for this problem: the 256-row kernel's
+// stream-K (M >= 1024), else the 128-row kernel's split-K.
 int64_t gemm_workspace_bytes(const Layout& L, int64_t M) {
-    return M >= kGemm256MinM ? gemm256_workspace_bytes(L, M) : 0;
+    if (M >= kGemm256MinM && gemm256_supported(L)) return gemm256_workspace_bytes(L, M);
+    if (!main_kernel_fits(L, L.bits)) return 0;
+    const SplitPlan sp = L.bits == 4 ? plan_split<4>(L, M) : plan_split<8>(L, M);
+    return split_workspace_bytes(L, M, sp);
 }
 
 int launch_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, size_t ws_bytes, hipStream_t s) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
     if (use_gemm256(L, M, ws)) return launch_gemm256(L, A, pk, C, M, ws, ws_bytes, s);
-    return L.bits == 4 ? launch_bits<4>(L, A, pk, C, M, s) : launch_bits<8>(L, A, pk, C, M, s);
+    // a workspace too small for this kernel's split (sized for another
+    // kernel of a larger M) selects the single-pass form
+    if (ws && (int64_t)ws_bytes < gemm_workspace_bytes(L, M)) ws = nullptr;
+    return L.bits == 4 ? launch_bits<4>(L, A, pk, C, M, ws, s) : launch_bits<8>(L, A, pk, C, M, ws, s);
 }
 
 }  // namespace tf

@@ -39,15 +39,6 @@ constexpr int kSkMinUnits = 8;         // fewest K chunks per stream-K block
 // over distinct bank groups.
 __device__ __forceinline__ int a_slot(int row, int ch) { return row * 4 + (ch ^ ((row >> 2) & 3)); }
 
-// Raw buffer resource over [base, base + bytes): loads past the end return 0.
-// Word 3 = 32-bit data format, no swizzle, for this GPU family.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-// Cache policy of the stream-K partials and counters: sc1, device-coherent
-// (writes reach memory visible to every XCD, reads do not hit a stale line).
-constexpr int kSc1 = 16;
 __device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }

@@ -54,8 +54,10 @@ struct GemvCfg {
     static constexpr int T = BITS == 4 ? 4 : 2;      // columns per lane
     static constexpr int PW = BITS == 4 ? 64 : 32;   // panel width
     static constexpr bool FACT = M <= kFactMaxM;
-    // 16 row slots (GEMM calls with few rows): matrix cores, A read per atom
+    // 16, 32 or 64 row slots (GEMM calls with few rows): matrix cores, A
+    // read per atom, MB blocks of 16 rows
     static constexpr bool MF = M > TF_GEMV_MAX_M;
+    static constexpr int MB = MF ? M / 16 : 1;
     static constexpr int XR = MF ? 1 : M;             // rows of x staged in LDS
     static constexpr int CR = FACT ? M : 1;           // rows of slice sums
 };
@@ -83,7 +85,8 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     constexpr int U = kGemvU, T = Cfg::T, PW = Cfg::PW;
     constexpr bool FACT = Cfg::FACT, MF = Cfg::MF;
     constexpr int NT = WAVES * 64;
-    static_assert(!MF || M == 16, "the matrix-core form holds exactly 16 rows");
+    static_assert(!MF || M == 16 || M == 32 || M == 64, "the matrix-core form holds 16, 32 or 64 rows");
+    constexpr int MB = Cfg::MB;
     static_assert(SEG == 0 || U % SEG == 0, "segments tile a round");
     static_assert(U % D == 0, "the load ring tiles a round");
     // metadata of the groups one round touches: U / SEG groups, or up to U
@@ -163,18 +166,23 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         return __builtin_nontemporal_load(wrun + (int64_t)min(aw0 + min(j, nw - 1), na - 1) * 64);
     };
     u32x4 ring[D];
-    // Matrix-core form: the A operand of v_mfma_f32_16x16x32_f16 for atom j,
-    // row c (row slots past mr repeat row mr - 1), k = 32 a + 8 kg + 0..7,
-    // read straight from global memory (A is small and stays in L2) through
-    // a ring of its own.
-    const uint16_t* arow = A + (int64_t)min(c, mr - 1) * K + 8 * kg;
-    auto load_afrag = [&](int j) {
-        return *reinterpret_cast<const u32x4*>(arow + (int64_t)min(aw0 + min(j, nw - 1), na - 1) * kAtomK);
-    };
-    u32x4 aring[MF ? D : 1];
-    float4_t macc[MF ? T : 1];          // lane (c, kg): rows 4 kg + 0..3, columns c + 16 t
+    // Matrix-core form: the A operand of v_mfma_f32_16x16x32_f16 for atom j
+    // and row block b, row 16 b + c (row slots past mr repeat row mr - 1),
+    // k = 32 a + 8 kg + 0..7, read straight from global memory (A is small
+    // and stays in L2) through a ring of its own.
+    const uint16_t* arow[MB];
 #pragma unroll
-    for (int t = 0; t < (MF ? T : 1); ++t) macc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < MB; ++b) arow[b] = A + (int64_t)min(16 * b + c, mr - 1) * K + 8 * kg;
+    auto load_afrag = [&](int b, int j) {
+        return *reinterpret_cast<const u32x4*>(arow[b] + (int64_t)min(aw0 + min(j, nw - 1), na - 1) * kAtomK);
+    };
+    u32x4 aring[MF ? MB : 1][MF ? D : 1];
+    // lane (c, kg) of block (b, t): rows 16 b + 4 kg + 0..3, column c + 16 t
+    float4_t macc[MF ? MB : 1][MF ? T : 1];
+#pragma unroll
+    for (int b = 0; b < (MF ? MB : 1); ++b)
+#pragma unroll
+        for (int t = 0; t < (MF ? T : 1); ++t) macc[b][t] = float4_t{0.f, 0.f, 0.f, 0.f};
 
     // One round r of the run.
     auto consume_round = [&](int r, Meta& mt) {
@@ -268,10 +276,13 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
             // take atom j from the ring and request atom j + D in its place
             const u32x4 wv = ring[i % D];
             ring[i % D] = load_atom(j + D);
-            u32x4 afrag;
+            u32x4 afrag[MF ? MB : 1];
             if constexpr (MF) {
-                afrag = aring[i % D];
-                aring[i % D] = load_afrag(j + D);
+#pragma unroll
+                for (int b = 0; b < MB; ++b) {
+                    afrag[b] = aring[b][i % D];
+                    aring[b][i % D] = load_afrag(b, j + D);
+                }
             }
             // dequant form, group size known at run time: this atom's metadata
             if constexpr (!FACT && SEG == 0) open();
@@ -305,8 +316,10 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                                                  : dq_w8_dwords(wd[2 * t], wd[2 * t + 1], nz[t], s2[t]);
                     if constexpr (MF) {
                         // the dequantized dword is the B operand of columns c + 16 t
-                        macc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                            __builtin_bit_cast(half8_t, afrag), w8, macc[t], 0, 0, 0);
+#pragma unroll
+                        for (int b = 0; b < MB; ++b)
+                            macc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                                __builtin_bit_cast(half8_t, afrag[b]), w8, macc[b][t], 0, 0, 0);
                         continue;
                     }
                     const u32x4 wu = __builtin_bit_cast(u32x4, w8);
@@ -349,7 +362,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 #pragma unroll
         for (int d = 0; d < D; ++d) {
             ring[d] = load_atom(d);
-            if constexpr (MF) aring[d] = load_afrag(d);
+            if constexpr (MF)
+#pragma unroll
+                for (int b = 0; b < MB; ++b) aring[b][d] = load_afrag(b, d);
         }
         // The next round's small loads are issued even past the last round,
         // at clamped addresses: without a branch around a load the compiler's
@@ -373,7 +388,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 #pragma unroll
         for (int t = 0; t < T; ++t)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) sm.red[wave][4 * kg + q][c + 16 * t] = macc[t][q];
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int b = 0; b < MB; ++b) sm.red[wave][16 * b + 4 * kg + q][c + 16 * t] = macc[b][t][q];
     } else {
         // Lanes c, c+16, c+32, c+48 hold the same columns: combine over kg.
 #pragma unroll
@@ -545,7 +562,12 @@ int64_t gemv_workspace_bytes(const Layout& L, int64_t M) {
     return M >= 1 && M <= TF_GEMV_MAX_M ? workspace_for_slots(L, M) : 0;
 }
 
-int64_t skinny_workspace_bytes(const Layout& L) { return workspace_for_slots(L, kSkinnyMaxM); }
+// row slots of the matrix-core form for M rows: 16, 32 or 64
+static int64_t skinny_slots(int64_t M) { return M <= 16 ? 16 : M <= 32 ? 32 : 64; }
+
+int64_t skinny_workspace_bytes(const Layout& L, int64_t M) {
+    return M >= 1 && M <= kSkinnyMaxM ? workspace_for_slots(L, skinny_slots(M)) : 0;
+}
 
 int launch_gemv(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, hipStream_t s) {
@@ -557,8 +579,14 @@ int launch_skinny_gemm(const Layout& L, const uint16_t* A, const void* packed, u
                        int64_t M, void* ws, hipStream_t s) {
     if (M < 1 || M > kSkinnyMaxM) return TF_ERR_ARG;
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    return L.bits == 4 ? launch_m<4, kSkinnyMaxM>(L, A, pk, C, ws, s, (int)M)
-                       : launch_m<8, kSkinnyMaxM>(L, A, pk, C, ws, s, (int)M);
+    switch (skinny_slots(M)) {
+        case 16: return L.bits == 4 ? launch_m<4, 16>(L, A, pk, C, ws, s, (int)M)
+                                    : launch_m<8, 16>(L, A, pk, C, ws, s, (int)M);
+        case 32: return L.bits == 4 ? launch_m<4, 32>(L, A, pk, C, ws, s, (int)M)
+                                    : launch_m<8, 32>(L, A, pk, C, ws, s, (int)M);
+        default: return L.bits == 4 ? launch_m<4, 64>(L, A, pk, C, ws, s, (int)M)
+                                    : launch_m<8, 64>(L, A, pk, C, ws, s, (int)M);
+    }
 }
 
 }  // namespace tf

@@ -49,9 +49,9 @@ constexpr int64_t kWsCounterBytes = (TF_MAX_DIM / 32) * 4;
 // Most workgroups a stream-K GEMM launch uses (sizes its workspace).
 constexpr int kSkMaxGroups = 256;
 // GEMM calls with kSkinnyMinM..kSkinnyMaxM rows run the streaming kernel's
-// matrix-core form (16 row slots); fewer rows run the decode GEMV.
+// matrix-core form (16, 32 or 64 row slots); fewer rows run the decode GEMV.
 constexpr int kSkinnyMinM = 4;
-constexpr int kSkinnyMaxM = 16;
+constexpr int kSkinnyMaxM = 64;
 constexpr int kAtomK = 32;
 constexpr int kAtomBytes = 1024;
 
@@ -113,6 +113,17 @@ typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 typedef float float2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer resource over [base, base + bytes): loads past the end return 0.
+// Word 3 = 32-bit data format, no swizzle, for this GPU family.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+// Cache policy of split-K partial sums: sc1, device-coherent (writes reach
+// memory visible to every XCD, reads do not hit a stale line).
+constexpr int kSc1 = 16;
 
 __device__ __forceinline__ half2_t as_h2(uint32_t v) { return __builtin_bit_cast(half2_t, v); }
 __device__ __forceinline__ uint32_t as_u32(half2_t v) { return __builtin_bit_cast(uint32_t, v); }
@@ -294,7 +305,7 @@ int launch_unpack(const Layout& L, const void* packed, uint8_t* q_out, uint8_t* 
 int launch_dequant(const Layout& L, const void* packed, int out_dtype, void* w_out,
                    hipStream_t s);
 int64_t gemv_workspace_bytes(const Layout& L, int64_t M);
-int64_t skinny_workspace_bytes(const Layout& L);
+int64_t skinny_workspace_bytes(const Layout& L, int64_t M);
 int launch_gemv(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, hipStream_t s);
 int launch_skinny_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C,

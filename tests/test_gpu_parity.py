@@ -165,7 +165,10 @@ GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 2
                (4, 12, 1024, 200, 64), (8, 16, 2048, 264, 128), (4, 13, 512, 1032, 32), (8, 10, 384, 40, 128),
                # 4..8 rows through the GEMM entry: the matrix-core streaming form
                (4, 4, 512, 136, 128), (8, 5, 384, 40, 32), (4, 8, 1024, 200, 64), (8, 7, 2048, 264, 128),
-               (4, 6, 288, 72, 96), (4, 3, 256, 64, 128)]
+               (4, 6, 288, 72, 96), (4, 3, 256, 64, 128),
+               # 17..64 rows: two or four row blocks of the streaming form
+               (4, 24, 1024, 520, 128), (8, 31, 512, 72, 64), (4, 48, 2048, 264, 32), (8, 64, 1024, 2056, 128),
+               (4, 40, 768, 136, 256)]
 
 
 @pytest.mark.parametrize("bits,M,K,N,G", GEMM_SHAPES)
@@ -178,7 +181,8 @@ def test_gemm_parity_small(tf, bits, M, K, N, G):
                                              ("gemm", 8, 256, 4096, 512), ("gemm", 4, 200, 8192, 256),
                                              ("gemv", 4, 1, 32768, 64), ("gemm", 4, 1030, 8192, 512),
                                              ("gemm", 8, 1024, 4096, 768), ("gemm", 4, 16, 4096, 1024),
-                                             ("gemm", 8, 5, 8192, 512)])
+                                             ("gemm", 8, 5, 8192, 512), ("gemm", 4, 64, 4096, 1024),
+                                             ("gemm", 8, 33, 4096, 520)])
 def test_integer_invariant_bitexact(tf, kind, bits, M, K, N):
     """s = 1, z = 0, integer x in [-3, 3]: every partial sum is an integer below
     2^24, so the fp16 output must be RNE of the exact integer matmul."""
@@ -254,11 +258,17 @@ def test_workspace_shared_across_shapes(tf):
 @pytest.mark.parametrize("bits,M,K,N,G", [(4, 16, 2048, 2048, 128), (8, 11, 4096, 520, 64),
                                            (4, 12, 16384, 512, 128), (8, 16, 14336, 1024, 128),
                                            (4, 1300, 2048, 1000, 128), (8, 1520, 1024, 776, 64),
-                                           (4, 2048, 1024, 4096, 32), (4, 1100, 3072, 2320, 128)])
+                                           (4, 2048, 1024, 4096, 32), (4, 1100, 3072, 2320, 128),
+                                           # 128-row tiles split along K (few tiles)
+                                           (8, 512, 4096, 4096, 128), (4, 100, 4096, 3000, 128),
+                                           (4, 300, 2048, 520, 64), (8, 40, 8192, 264, 32),
+                                           (4, 700, 1536, 1000, 128), (4, 64, 8192, 1024, 128),
+                                           (8, 40, 4096, 4096, 128)])
 def test_gemm_workspace_modes(tf, bits, M, K, N, G):
-    """The stream-K split (workspace) and the whole-tile kernels (no workspace)
-    both meet the bar; a stream-K result is bitwise repeatable and its
-    workspace serves the next call at once."""
+    """The K-split kernels (workspace: stream-K for 256-row tiles, split-K for
+    128-row tiles) and the whole-tile kernels (no workspace) both meet the
+    bar; a split result is bitwise repeatable and its workspace serves the
+    next call at once."""
     d = make_inputs(bits, M, K, N, group=G, seed=M + N)
     packed = pack(tf, d)
     want = ref(d)
@@ -275,7 +285,8 @@ def test_gemm_workspace_modes(tf, bits, M, K, N, G):
 def test_workspace_shared_gemm_gemv(tf):
     """One workspace serves split-K GEMVs and stream-K GEMMs in turn."""
     cases = [("gemm", 4, 1300, 1024, 1000), ("gemv", 4, 1, 14336, 4096), ("gemm", 8, 1600, 2048, 520),
-             ("gemv", 8, 3, 8192, 520), ("gemm", 4, 1300, 1024, 1000)]
+             ("gemv", 8, 3, 8192, 520), ("gemm", 4, 1300, 1024, 1000), ("gemm", 8, 300, 4096, 1024),
+             ("gemm", 4, 12, 8192, 512), ("gemm", 4, 200, 2048, 2000)]
     need = max(tf.workspace_bytes(b, m, k, n) for _, b, m, k, n in cases)
     ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
     for i, (kind, bits, M, K, N) in enumerate(cases):
