@@ -47,6 +47,10 @@ __device__ __forceinline__ int a_slot(int row, int ch) { return row * 4 + (ch ^ 
 
 // MPC: metadata groups per chunk (1 when a group spans the whole chunk, else
 // chunk rows / group); the group of step j is j / (chunk steps / MPC).
+// Most K slices per tile (the finishing slice holds the other slices' parts
+// of one row block in registers).
+constexpr int kMaxSplit = 4;
+
 // Split-K arguments: S slices per tile of cps chunks each (S = 1: no split);
 // arrival counters (zero at rest) and partial tiles in the workspace.
 struct SplitK {
@@ -251,22 +255,19 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
     }
 
     // ---- epilogue: lane holds column c of each 16x16 block, rows 4 kg + r
-    auto store = [&](auto&& total_of) {
+    auto store_block = [&](int i, int t, const float4_t& v) {
+        const int64_t col = col0 + 16 * t + c;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t row = row0 + 16 * i + 4 * kg + r;
+            if (row < M && col < N) C[row * N + col] = __builtin_bit_cast(uint16_t, (_Float16)v[r]);
+        }
+    };
+    if (sk.S == 1) {
 #pragma unroll
         for (int i = 0; i < 8; ++i)
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const float4_t v = total_of(i, t);
-                const int64_t col = col0 + 16 * t + c;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int64_t row = row0 + 16 * i + 4 * kg + r;
-                    if (row < M && col < N) C[row * N + col] = __builtin_bit_cast(uint16_t, (_Float16)v[r]);
-                }
-            }
-    };
-    if (sk.S == 1) {
-        store([&](int i, int t) { return acc[i][t]; });
+            for (int t = 0; t < 4; ++t) store_block(i, t, acc[i][t]);
         return;
     }
     // Park this slice's partial tile (wave w's 128 x 64 part, block (i, t) as
@@ -294,18 +295,30 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
     __syncthreads();
     if (!last) return;
     // The last slice adds the tile's slices in order: those before it, its
-    // own from registers, those after it.
-    store([&](int i, int t) {
-        const uint32_t off = (uint32_t)(((i * 4 + t) * 64 + lane) * 16);
-        float4_t r = {0.f, 0.f, 0.f, 0.f};
-        for (int sl = 0; sl < sk.S; ++sl) {
-            if (sl == split)
-                r += acc[i][t];
-            else
-                r += __builtin_bit_cast(float4_t, __builtin_amdgcn_raw_buffer_load_b128(part_rsrc(sl), off, 0, kSc1));
+    // own from registers, those after it.  The other slices' parts of one row
+    // block are all requested before any is used, so the block costs one
+    // memory latency, not one per (slice, column block).
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float4_t p[kMaxSplit][4];
+#pragma unroll
+        for (int sl = 0; sl < kMaxSplit; ++sl)
+            if (sl < sk.S && sl != split) {
+                const __amdgpu_buffer_rsrc_t pr = part_rsrc(sl);
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    p[sl][t] = __builtin_bit_cast(float4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                                pr, (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, kSc1));
+            }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            float4_t r = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int sl = 0; sl < kMaxSplit; ++sl)
+                if (sl < sk.S) r += sl == split ? acc[i][t] : p[sl][t];
+            store_block(i, t, r);
         }
-        return r;
-    });
+    }
     if (tid == 0)   // leave the counter at zero for the next call
         __hip_atomic_store(&sk.cnt[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -415,15 +428,13 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_generic(
 }
 
 // Split plan of the main kernel: K is cut only when a workspace is given and
-// the tiles are fewer than kSplitBelowTiles; slices keep at least
-// kMinSliceChunks chunks.  Aiming at about 128 units (rather than one per
-// compute unit) measured fastest on MI355X: the slice that finishes a tile
-// reads the others' partial tiles alone, at one compute unit's rate.
+// the tiles are fewer than kSplitBelowTiles, into at most kMaxSplit slices of
+// at least kMinSliceChunks chunks, aiming at one unit per compute unit.
 struct SplitPlan {
     int S, cps;
 };
 constexpr int kSplitBelowTiles = 256;
-constexpr int kTargetUnits = 128;
+constexpr int kTargetUnits = 256;
 constexpr int kMinSliceChunks = 4;
 
 template <int BITS>
@@ -433,7 +444,7 @@ SplitPlan plan_split(const Layout& L, int64_t M) {
     int S = 1;
     if (tiles < kSplitBelowTiles) {
         S = (int)std::min<int64_t>((kTargetUnits + tiles - 1) / tiles, chunks / kMinSliceChunks);
-        S = std::max(S, 1);
+        S = std::max(std::min(S, kMaxSplit), 1);
     }
     const int cps = (chunks + S - 1) / S;
     return {(chunks + cps - 1) / cps, cps};    // no empty slice

@@ -93,6 +93,10 @@ __device__ __forceinline__ void barrier_after_a_loads() {
 // last), writes C and returns the counter to zero.  Partials and counters are
 // accessed with device-coherent (sc1) loads and stores: the blocks of one
 // tile run on different XCDs, whose L2 caches are not coherent.
+// Other segments whose partial row block the finishing block holds in
+// registers at once.
+constexpr int kMaxParts = 3;
+
 struct StreamK {
     int groups;               // G, 0 = data-parallel
     int units;                // tiles * chunks
@@ -188,16 +192,21 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     // rows per store instruction.  get(i, t) yields accumulator block (i, t):
     // row m = 16 i + c, columns n = 16 t + 4 kg + 0..3 of the wave's tile.
     // The caller has made sure no wave still reads the A buffers underneath.
-    auto store_tile = [&](int64_t row0, int64_t col0, auto&& get) {
+    auto store_tile = [&](int64_t row0, int64_t col0, auto&& get_block) {
         uint8_t* stage = reinterpret_cast<uint8_t*>(As0) + wave * 4096;
         constexpr int kStageRow = 144;
         const bool interior = row0 + kBM <= M && col0 + 64 <= N;
         const int rr = lane >> 3, cc = lane & 7;      // read-back: row rr (+8), 16-byte chunk cc
 #pragma unroll
         for (int i = 0; i < kRB; ++i) {
+            // one row block at a time: keep the scheduler from hoisting the
+            // loads of every block (their registers would not fit)
+            __builtin_amdgcn_sched_barrier(0);
+            float4_t blk[4];
+            get_block(i, blk);
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                const float4_t a = get(i, t);
+                const float4_t a = blk[t];
                 const half2_t lo = {(_Float16)a[0], (_Float16)a[1]};
                 const half2_t hi = {(_Float16)a[2], (_Float16)a[3]};
                 *reinterpret_cast<uint2*>(stage + c * kStageRow + 32 * t + 8 * kg) = uint2{as_u32(lo), as_u32(hi)};
@@ -390,7 +399,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         ua = sk_begin(v, G, U);
         ub = sk_begin(v + 1, G, U);
     }
-    auto whole = [&](int i, int t) { return acc[i][t]; };
+    auto whole = [&](int i, float4_t (&blk)[4]) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) blk[t] = acc[i][t];
+    };
     int64_t row0, col0;
     for (int u = ua; u < ub;) {
         const int tile = u / chunks, c0 = u % chunks;
@@ -419,24 +431,55 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                             (uint32_t)(vhi - vlo);
             __syncthreads();
             if (last_flag) {
-                // Sum the segments in K order (block vlo first): the partials
-                // of the blocks before this one, this block's own from its
-                // registers, then those after it.
-                auto partial_of = [&](int w, int i, int t) {
+                // Sum the segments' parts in K order (block vlo first).  This
+                // block's own part is read back too (it was just parked), so
+                // the sum needs no accumulator registers; the parts of one row
+                // block are all requested before any is used (one memory
+                // latency per row block, not one per segment and column
+                // block).  More than kMaxParts + 1 segments take the
+                // one-by-one path.
+                const int nb = vhi - vlo;
+                __amdgpu_buffer_rsrc_t prs[kMaxParts + 1];     // segment vlo + j's part
+#pragma unroll
+                for (int j = 0; j <= kMaxParts; ++j) {
+                    const int w = min(vlo + j, vhi);
                     const int sw = 2 * w + (sk_begin(w, G, U) >= t0 ? 0 : 1);
-                    const __amdgpu_buffer_rsrc_t q =
-                        make_rsrc(sk.part + (int64_t)sw * (kBM * kBN) + wave * (kBM * 64), kBM * 64 * 4);
+                    prs[j] = make_rsrc(sk.part + (int64_t)sw * (kBM * kBN) + wave * (kBM * 64), kBM * 64 * 4);
+                }
+                auto part_of = [&](const __amdgpu_buffer_rsrc_t& q, int i, int t) {
                     return __builtin_bit_cast(float4_t, __builtin_amdgcn_raw_buffer_load_b128(
                                                             q, (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, kSc1));
                 };
-                auto total_of = [&](int i, int t) {
-                    float4_t r = {0.f, 0.f, 0.f, 0.f};
-                    for (int w = vlo; w < v; ++w) r += partial_of(w, i, t);
-                    r += acc[i][t];
-                    for (int w = v + 1; w <= vhi; ++w) r += partial_of(w, i, t);
-                    return r;
+                auto total_block = [&](int i, float4_t (&blk)[4]) {
+                    if (nb <= kMaxParts) {
+                        float4_t p[kMaxParts + 1][4];
+#pragma unroll
+                        for (int j = 0; j <= kMaxParts; ++j)
+                            if (j <= nb)
+#pragma unroll
+                                for (int t = 0; t < 4; ++t) p[j][t] = part_of(prs[j], i, t);
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) {
+                            float4_t r = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                            for (int j = 0; j <= kMaxParts; ++j)
+                                if (j <= nb) r += p[j][t];
+                            blk[t] = r;
+                        }
+                        return;
+                    }
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        float4_t r = {0.f, 0.f, 0.f, 0.f};
+                        for (int w = vlo; w <= vhi; ++w) {
+                            const int sw = 2 * w + (sk_begin(w, G, U) >= t0 ? 0 : 1);
+                            r += part_of(make_rsrc(sk.part + (int64_t)sw * (kBM * kBN) + wave * (kBM * 64),
+                                                   kBM * 64 * 4), i, t);
+                        }
+                        blk[t] = r;
+                    }
                 };
-                store_tile(row0, col0, total_of);
+                store_tile(row0, col0, total_block);
                 if (tid == 0) __hip_atomic_store(&sk.cnt[vlo], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
