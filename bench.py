@@ -76,6 +76,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--msweep", action="store_true",
+                    help="the M sweep (256..8192 step 256) at both Llama MLP shapes, one JSON line each")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the step, time every synthetic workload configuration "
                          "(one JSON line each)")
@@ -197,6 +199,54 @@ def sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps)
     del g
 
 
+def msweep(torch, tf, make_inputs, target_ms=6.0):
+    """The paper's prompt-length sweep: W4A16 GEMM for M = 256..8192 (step
+    256) at (K, N) = (4096, 14336) and (14336, 4096).  Per shape one input
+    draw at M = 8192 (each M takes its first M rows of A) and enough copies of
+    the packed weight to stream it from HBM; HIP-graph replay as in --sweep,
+    with about `target_ms` of GPU time per graph."""
+    from paper_2606_11357_amd.synth import M_SWEEP, M_SWEEP_SHAPES
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    for (K, N) in M_SWEEP_SHAPES:
+        d = make_inputs(4, max(M_SWEEP), K, N, group=GROUP, seed=0)
+        p0 = tf.pack_w4(up(d["qweight"]), up(d["qzeros"]), up(d["s"]), K, N, GROUP)
+        ncopy = int(min(24, max(2, -(-(512 << 20) // p0.numel()))))
+        copies = [p0] + [p0.clone() for _ in range(ncopy - 1)]
+        xall = up(d["x"])
+        del d
+        for M in M_SWEEP:
+            x = xall[:M]
+            y = torch.empty((M, N), dtype=torch.float16, device=dev)
+            flops = 2.0 * M * N * K
+            reps = int(max(4, min(50, target_ms * 1e-3 / (flops / 1.0e15))))
+            for i in range(3):
+                tf.w4a16_gemm(x, copies[i % ncopy], K, N, GROUP, out=y)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for i in range(reps):
+                    tf.w4a16_gemm(x, copies[i % ncopy], K, N, GROUP, out=y)
+            g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(3):
+                g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / (3 * reps)
+            tflops = flops / us / 1e6
+            print(json.dumps({"workload": "w4a16_gemm_msweep", "M": M, "K": K, "N": N, "group": GROUP,
+                              "us_per_launch": round(us, 3), "TFLOP/s": round(tflops, 2),
+                              "frac": round(tflops / PEAK_F16_TFLOPS, 4), "launches": 3 * reps,
+                              "weight_copies": ncopy, "timing": "HIP graph replay"}), flush=True)
+            del g, y
+        del copies, p0, xall
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -217,6 +267,9 @@ def main():
     tf.load()
     if args.sweep:
         sweep(torch, tf, make_inputs)
+        return
+    if args.msweep:
+        msweep(torch, tf, make_inputs)
         return
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)

@@ -33,6 +33,8 @@ __all__ = [
     "make_inputs",
     "make_inputs_w8sym",
     "WORKLOADS",
+    "M_SWEEP",
+    "M_SWEEP_SHAPES",
 ]
 
 
@@ -104,6 +106,11 @@ def make_inputs_w8sym(M: int, K: int, N: int, seed: int = 0, x_std: float = 1.0,
 
 # The synthetic Llama-shaped workloads the library is measured and checked on.
 # Each entry: name -> (bits, M values, K, N, x_std).  Scale ranges follow bits.
+# The paper's GEMM sweep (Section 5: prompt lengths M from 256 to 8192 in steps
+# of 256 at both Llama-3-8B MLP shapes, K and N swapped), W4A16, G = 128.
+M_SWEEP = tuple(range(256, 8192 + 1, 256))
+M_SWEEP_SHAPES = ((4096, 14336), (14336, 4096))
+
 WORKLOADS = {
     "w4_gemm_m16_k2048_n2048": (4, (16,), 2048, 2048, 1.0),
     "w4_gemv_k4096_n14336": (4, (1, 4, 8), 4096, 14336, 1.0),

@@ -344,3 +344,21 @@ def test_gemm_w4_large_sampled(tf, M, K, N, xstd):
     cols = np.unique(cols)
     want = ref(d, x=d["x"][rows], cols=cols)
     assert_parity(got[np.ix_(rows, cols)], want, f"W4 GEMM {M}x{K}x{N} sampled")
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("M", [256, 1280, 4352, 8192])
+@pytest.mark.parametrize("K,N", [(4096, 14336), (14336, 4096)])
+def test_gemm_w4_msweep_sampled(tf, M, K, N):
+    """Points of the paper's prompt-length sweep (M = 256..8192 step 256, both
+    Llama-3-8B MLP shapes) at full size: sampled rows x columns against the
+    oracle, all of C finite.  Covers the 128-row split-K kernel (M = 256), the
+    256-row kernel in whole-tile and stream-K forms and the largest M."""
+    d = make_inputs(4, M, K, N, seed=M)
+    got = run(tf, "gemm", d, pack(tf, d))
+    assert np.all(np.isfinite(got.astype(np.float64)))
+    rng = np.random.default_rng(M + K)
+    rows = np.unique(np.concatenate([[0, M - 1], rng.choice(M, size=24, replace=False)]))
+    cols = np.unique(np.concatenate([[0, N - 1], _sample_cols(N, rng, 254)]))
+    want = ref(d, x=d["x"][rows], cols=cols)
+    assert_parity(got[np.ix_(rows, cols)], want, f"W4 GEMM sweep {M}x{K}x{N} sampled")
