@@ -102,6 +102,7 @@ struct StreamK {
     int units;                // tiles * chunks
     uint32_t* cnt;            // G arrival counters (zero at rest)
     float* part;              // 2 G partial tiles of kBM x kBN floats
+    int dp_rounds;            // hybrid: whole tiles per block before the stream-K units
 };
 
 __device__ __forceinline__ int sk_owner(int64_t u, int G, int U) {   // block whose range holds u
@@ -381,39 +382,58 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         __syncthreads();   // every wave done with the A buffers (the output staging reuses them)
     };
 
-    // Range of 128-row K chunks ("units", tile-major) this block computes.
+    // Work of this block: whole tiles first, then a range [ua, ub) of 128-row
+    // K chunks ("units", tile-major) of the stream-K part.
     const int G = sk.groups, U = sk.units, b = blockIdx.x;
-    int v = 0, ua, ub;
+    int v = 0, ua = 0, ub = 0, nwhole, dpu = 0;
+    int dp_tile0;                  // data-parallel: this block's tile
     if (G == 0) {
         // Data-parallel: XCD band of the tile list; block b runs on XCD b % 8
         // and takes the (b / 8)-th tile of that XCD's contiguous band.
         const int total = tiles_m * tiles_n;
         const int per = total / kXcds, rem = total % kXcds;
         const int x = b % kXcds, i = b / kXcds;
-        ua = (x * per + min(x, rem) + i) * chunks;
-        ub = ua + chunks;
+        dp_tile0 = x * per + min(x, rem) + i;
+        nwhole = 1;
     } else {
         // Stream-K: virtual block index v numbers the blocks XCD by XCD, so
-        // each XCD walks a contiguous part of the unit list.
+        // each XCD walks a contiguous part of the unit list.  Hybrid: the
+        // first dp_rounds * G tiles go whole, tile r * G + v to block v, and
+        // the stream-K units cover the tiles after them.
         v = (G % kXcds == 0) ? (b % kXcds) * (G / kXcds) + b / kXcds : b;
-        ua = sk_begin(v, G, U);
-        ub = sk_begin(v + 1, G, U);
+        nwhole = sk.dp_rounds;
+        dp_tile0 = v;
+        dpu = sk.dp_rounds * G * chunks;
+        ua = dpu + sk_begin(v, G, U);
+        ub = dpu + sk_begin(v + 1, G, U);
     }
     auto whole = [&](int i, float4_t (&blk)[4]) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) blk[t] = acc[i][t];
     };
     int64_t row0, col0;
-    for (int u = ua; u < ub;) {
-        const int tile = u / chunks, c0 = u % chunks;
-        const int c1 = min(chunks, c0 + (ub - u));
+    // (one call site of `segment`, whose body is large)
+    for (int k = 0, u = ua; k < nwhole || u < ub;) {
+        int tile, c0, c1;
+        const int useg = u;                               // first unit of a stream-K segment
+        if (k < nwhole) {
+            tile = dp_tile0 + k * G;
+            c0 = 0;
+            c1 = chunks;
+            ++k;
+        } else {
+            tile = u / chunks;
+            c0 = u % chunks;
+            c1 = min(chunks, c0 + (ub - u));
+            u += c1 - c0;
+        }
         segment(tile, c0, c1, row0, col0);
         if (c0 == 0 && c1 == chunks) {
             store_tile(row0, col0, whole);
         } else {
             // Park the partial: wave w's 256 x 64 part at w * 16384 floats,
             // block (i, t) as 64 consecutive float4 (one per lane).
-            const int slot = 2 * v + (u == ua ? 0 : 1);
+            const int slot = 2 * v + (useg == ua ? 0 : 1);
             float* part = sk.part + (int64_t)slot * (kBM * kBN);
             const __amdgpu_buffer_rsrc_t pr = make_rsrc(part + wave * (kBM * 64), kBM * 64 * 4);
 #pragma unroll
@@ -424,7 +444,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                                                            (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, kSc1);
             __builtin_amdgcn_s_waitcnt(0);                // this thread's partial stores have completed
             __syncthreads();
-            const int t0 = tile * chunks;
+            const int t0 = tile * chunks - dpu;            // the tile's first unit, stream-K numbering
             const int vlo = sk_owner(t0, G, U), vhi = sk_owner(t0 + chunks - 1, G, U);
             if (tid == 0)
                 last_flag = __hip_atomic_fetch_add(&sk.cnt[vlo], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
@@ -483,7 +503,6 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                 if (tid == 0) __hip_atomic_store(&sk.cnt[vlo], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
-        u += c1 - c0;
     }
 }
 
@@ -538,18 +557,33 @@ int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16
     const int tiles = tiles_m * tiles_n, chunks = (int)(L.K / (kBK * kCS));
     const int64_t need = gemm256_workspace_bytes(L, M);
     const int cus = device_cus();
-    StreamK sk{0, 0, nullptr, nullptr};
-    // Whole tiles while they keep at least 80% of the launch's block slots busy
-    // (ceil(tiles / cus) waves of cus blocks), stream-K below that, with at
-    // least kSkMinUnits K chunks per block.
+    StreamK sk{0, 0, nullptr, nullptr, 0};
+    // Otherwise (with a workspace) stream-K, with at least kSkMinUnits K
+    // chunks per block.  With at least one full wave of tiles the full waves
+    // stay whole tiles and only the tiles after them are split ("hybrid"):
+    // fewer partial tiles than splitting everything, no idle units in the
+    // last wave.
+    // Whole tiles while they keep at least 80% of the launch's block slots
+    // busy (ceil(tiles / cus) waves of cus blocks); measured on MI355X over
+    // the M = 256..8192 sweep, the hybrid below loses to whole tiles there.
     const int64_t waves = (tiles + cus - 1) / cus;
     const bool dp_ok = 5 * (int64_t)tiles >= 4 * waves * cus;
     if (ws && need > 0 && (int64_t)ws_bytes >= need && !dp_ok) {
-        const int64_t units = (int64_t)tiles * chunks;
-        int G = (int)std::min<int64_t>(std::min(cus, kSkMaxGroups), std::max<int64_t>(1, units / kSkMinUnits));
+        int G = std::min(cus, kSkMaxGroups);
+        if (G > kXcds) G -= G % kXcds;
+        int dp_rounds = tiles / G;
+        // the stream-K part keeps at least kSkMinUnits chunks per block: a
+        // short remainder joins the last whole wave
+        if (dp_rounds > 0 && (int64_t)(tiles - dp_rounds * G) * chunks < (int64_t)G * kSkMinUnits) --dp_rounds;
+        // and cuts each of its tiles into at most kMaxParts + 1 segments (the
+        // finishing block's fast path); otherwise everything is split
+        if (dp_rounds > 0 && (int64_t)(tiles - dp_rounds * G) * chunks * kMaxParts < (int64_t)G * chunks)
+            dp_rounds = 0;
+        const int64_t units = (int64_t)(tiles - dp_rounds * G) * chunks;
+        if (dp_rounds == 0) G = (int)std::min<int64_t>(G, std::max<int64_t>(1, units / kSkMinUnits));
         if (G > kXcds) G -= G % kXcds;
         sk = StreamK{G, (int)units, static_cast<uint32_t*>(ws),
-                     reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes)};
+                     reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes), dp_rounds};
     }
     const int chunk_rows = kBK * kCS;
     const int mpc = L.group >= chunk_rows ? 1 : chunk_rows / L.group;
