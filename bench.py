@@ -76,6 +76,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--context", action="store_true",
+                    help="reference points only: dense fp16 torch.matmul on the prefill shapes and a "
+                         "device copy of the decode GEMV's byte count")
     ap.add_argument("--msweep", action="store_true",
                     help="the M sweep (256..8192 step 256) at both Llama MLP shapes, one JSON line each")
     ap.add_argument("--sweep", action="store_true",
@@ -199,6 +202,54 @@ def sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps)
     del g
 
 
+def graph_time_us(torch, fn, reps):
+    """Mean µs per call of fn() over 3 replays of a HIP graph of `reps` calls."""
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        fn(0)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(reps):
+            fn(i)
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(3):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / (3 * reps)
+
+
+def context(torch):
+    """Achievable-ceiling references, not targets: torch.matmul in fp16 (the
+    weights already dequantized to a dense fp16 [K, N]) on the two prefill
+    shapes, and a device copy of the decode GEMV's packed-weight byte count,
+    rotating over sources so it streams from HBM."""
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev).manual_seed(0)
+    for (M, K, N) in GEMM_SHAPES:
+        a = torch.randn((M, K), device=dev, dtype=torch.float16, generator=gen)
+        ws = [torch.randn((K, N), device=dev, dtype=torch.float16, generator=gen) * 0.02 for _ in range(4)]
+        out = torch.empty((M, N), device=dev, dtype=torch.float16)
+        us = graph_time_us(torch, lambda i: torch.matmul(a, ws[i % 4], out=out), 20)
+        print(json.dumps({"reference": "torch.matmul fp16 (hipBLASLt), dense fp16 weights", "M": M, "K": K,
+                          "N": N, "us_per_launch": round(us, 3),
+                          "TFLOP/s": round(2.0 * M * N * K / us / 1e6, 2)}), flush=True)
+        del a, ws, out
+    nbytes = algo_bytes_w4(GEMV_SHAPE[1], GEMV_SHAPE[2])
+    ncopy = -(-(512 << 20) // nbytes)
+    bufs = [torch.empty(nbytes, device=dev, dtype=torch.uint8) for _ in range(ncopy)]
+    dst = torch.empty(nbytes, device=dev, dtype=torch.uint8)
+    us = graph_time_us(torch, lambda i: dst.copy_(bufs[i % ncopy]), 64)
+    print(json.dumps({"reference": "device copy (torch copy_) of the decode GEMV's byte count",
+                      "bytes_read": nbytes, "bytes_written": nbytes, "copies": ncopy,
+                      "us_per_launch": round(us, 3), "read_GB/s": round(nbytes / us / 1e3, 1),
+                      "read+write_GB/s": round(2 * nbytes / us / 1e3, 1)}), flush=True)
+
+
 def msweep(torch, tf, make_inputs, target_ms=6.0):
     """The paper's prompt-length sweep: W4A16 GEMM for M = 256..8192 (step
     256) at (K, N) = (4096, 14336) and (14336, 4096).  Per shape one input
@@ -263,6 +314,9 @@ def main():
         sys.exit(1)
     if args.calibrate_copy:
         calibrate_copy(torch)
+        return
+    if args.context:
+        context(torch)
         return
     tf.load()
     if args.sweep:
