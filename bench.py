@@ -79,6 +79,8 @@ def parse():
     ap.add_argument("--context", action="store_true",
                     help="reference points only: dense fp16 torch.matmul on the prefill shapes and a "
                          "device copy of the decode GEMV's byte count")
+    ap.add_argument("--mlp", action="store_true",
+                    help="Llama-3-8B MLP composite (gate/up GEMM, silu*up, down GEMM) per stage and whole")
     ap.add_argument("--msweep", action="store_true",
                     help="the M sweep (256..8192 step 256) at both Llama MLP shapes, one JSON line each")
     ap.add_argument("--sweep", action="store_true",
@@ -250,6 +252,51 @@ def context(torch):
                       "read+write_GB/s": round(2 * nbytes / us / 1e3, 1)}), flush=True)
 
 
+def mlp(torch, tf, make_inputs, Ms=(1, 16, 256, 2048, 8192)):
+    """A Llama-3-8B MLP layer (hidden 4096, intermediate 14336) around the fused
+    matmul: one W4A16 GEMM for gate and up (weights concatenated along N,
+    N = 28672), tf_silu_mul, one W4A16 GEMM for down (K = 14336); synthetic
+    weights, G = 128.  Each stage and the whole layer timed by HIP-graph
+    replay (weights used in place: 4 bytes per parameter less than fp16, and
+    the 90 MB of packed weights partly stay in the 256 MB MALL across
+    replays)."""
+    dev = torch.device("cuda:0")
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    H, I = 4096, 14336
+    gu = make_inputs(4, max(Ms), H, 2 * I, group=GROUP, seed=0)
+    dn = make_inputs(4, 1, I, H, group=GROUP, seed=1)
+    p_gu = tf.pack_w4(up(gu["qweight"]), up(gu["qzeros"]), up(gu["s"]), H, 2 * I, GROUP)
+    p_dn = tf.pack_w4(up(dn["qweight"]), up(dn["qzeros"]), up(dn["s"]), I, H, GROUP)
+    xall = up(gu["x"])
+    del gu, dn
+    for M in Ms:
+        x = xall[:M]
+        g = torch.empty((M, 2 * I), dtype=torch.float16, device=dev)
+        h = torch.empty((M, I), dtype=torch.float16, device=dev)
+        y = torch.empty((M, H), dtype=torch.float16, device=dev)
+        gemm_or_gemv = tf.w4a16_gemv if M <= tf.GEMV_MAX_M else tf.w4a16_gemm
+        s1 = lambda i: gemm_or_gemv(x, p_gu, H, 2 * I, GROUP, out=g)
+        s2 = lambda i: tf.silu_mul(g, out=h)
+        s3 = lambda i: gemm_or_gemv(h, p_dn, I, H, GROUP, out=y)
+
+        def layer(i):
+            s1(i)
+            s2(i)
+            s3(i)
+        flops = 2.0 * M * (H * 2 * I + I * H)
+        reps = int(max(4, min(50, 5e-3 / max(flops / 1.0e15, 8e-6))))
+        t = [graph_time_us(torch, f, reps) for f in (s1, s2, s3, layer)]
+        print(json.dumps({"workload": "llama3_8b_mlp_w4a16", "M": M, "hidden": H, "intermediate": I,
+                          "entry": "gemv" if M <= tf.GEMV_MAX_M else "gemm",
+                          "us_gate_up": round(t[0], 3), "us_silu_mul": round(t[1], 3),
+                          "us_down": round(t[2], 3), "us_layer": round(t[3], 3),
+                          "TFLOP/s_layer": round(flops / t[3] / 1e6, 2),
+                          "matmul_share": round((t[0] + t[2]) / (t[0] + t[1] + t[2]), 4),
+                          "timing": "HIP graph replay"}), flush=True)
+        del g, h, y
+    torch.cuda.empty_cache()
+
+
 def msweep(torch, tf, make_inputs, target_ms=6.0):
     """The paper's prompt-length sweep: W4A16 GEMM for M = 256..8192 (step
     256) at (K, N) = (4096, 14336) and (14336, 4096).  Per shape one input
@@ -324,6 +371,9 @@ def main():
         return
     if args.msweep:
         msweep(torch, tf, make_inputs)
+        return
+    if args.mlp:
+        mlp(torch, tf, make_inputs)
         return
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)

@@ -177,6 +177,19 @@ int tf_unpack(int bits, const void* packed, int64_t K, int64_t N, int group,
 int tf_dequant(int bits, const void* packed, int64_t K, int64_t N, int group,
                int out_dtype, void* W_out, void* stream);
 
+/*
+ * Gated activation of a transformer MLP, for a layer-level composite around
+ * the matmuls (gate/up GEMM -> this -> down GEMM); not part of the paper's
+ * method:
+ *   H[m, n] = silu(G[m, n]) * U[m, n],   silu(g) = g / (1 + exp(-g)),
+ * where G = GU[:, 0:N] and U = GU[:, N:2N] are the two halves of one fp16
+ * [M, 2N] row-major matrix (the output of a GEMM whose weight concatenates
+ * the gate and up projections along N).  Computed in fp32; H is fp16 [M, N]
+ * row-major, rounded to nearest even.  Requires N % 8 == 0 and 16-byte
+ * aligned pointers; H must not overlap GU.
+ */
+int tf_silu_mul(const uint16_t* GU_f16, int64_t M, int64_t N, uint16_t* H_f16, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -15,3 +15,4 @@ from .awq_oracle import (  # noqa: F401
     w8a16,
     w8a16_sym,
 )
+from .mlp_oracle import mlp_w4a16, silu, silu_mul  # noqa: F401

@@ -179,4 +179,11 @@ int tf_dequant(int bits, const void* packed, int64_t K, int64_t N, int group, in
                               static_cast<hipStream_t>(stream));
 }
 
+int tf_silu_mul(const uint16_t* GU_f16, int64_t M, int64_t N, uint16_t* H_f16, void* stream) {
+    if (!GU_f16 || !H_f16) return TF_ERR_NULL;
+    if (M < 1 || M > TF_MAX_M || N <= 0 || N > TF_MAX_DIM || N % 8 != 0) return TF_ERR_SHAPE;
+    if (misaligned(GU_f16) || misaligned(H_f16)) return TF_ERR_ALIGN;
+    return tf::launch_silu_mul(GU_f16, M, N, H_f16, static_cast<hipStream_t>(stream));
+}
+
 }  // extern "C"

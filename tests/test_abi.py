@@ -204,3 +204,12 @@ def test_binding_refuses_cpu_tensors():
     x = torch.zeros(4, 256, dtype=torch.float16)
     with pytest.raises(ValueError):
         tfb.w4a16_gemv(x, torch.zeros(16, dtype=torch.uint8), 256, 64)
+
+
+@pytest.mark.parametrize("args,want", [
+    ((NULL, 4, 64, P, NULL), tfb.TF_ERR_NULL), ((P, 4, 64, NULL, NULL), tfb.TF_ERR_NULL),
+    ((P, 0, 64, P, NULL), tfb.TF_ERR_SHAPE), ((P, 4, 60, P, NULL), tfb.TF_ERR_SHAPE),
+    ((P, 4, 0, P, NULL), tfb.TF_ERR_SHAPE), ((P_ODD, 4, 64, P, NULL), tfb.TF_ERR_ALIGN),
+    ((P, 4, 64, P_ODD, NULL), tfb.TF_ERR_ALIGN)])
+def test_silu_mul_rejects(lib, args, want):
+    assert lib.tf_silu_mul(*args) == want
