@@ -37,6 +37,7 @@ GEMM_SHAPES = [(2048, 4096, 14336), (2048, 14336, 4096)]
 GEMV_SHAPE = (1, 4096, 14336)
 GROUP = 128
 GEMV_REPS = 32
+GEMM_COPIES = 8
 PEAK_F16_TFLOPS = 2516.6      # 256 CU x 4096 FLOP/clk x 2.4 GHz (dense fp16 MFMA)
 PEAK_HBM_GBS = 8000.0
 COPY_BYTES = 1 << 30
@@ -71,8 +72,8 @@ def recorded_traffic(kernel_file):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
@@ -385,12 +386,14 @@ def main():
         return tf.pack_w4(upload(d["qweight"]), upload(d["qzeros"]), upload(d["s"]),
                           d["K"], d["N"], GROUP)
 
-    # ---- inputs (offline: generation + pack are outside the timed region)
+    # ---- inputs (offline: generation + pack are outside the timed region);
+    # GEMM_COPIES copies of each prefill weight (about 490 MB in all, more than
+    # the 256 MB MALL), so the GEMMs stream their weights from HBM
     gemm = []
     for (M, K, N) in GEMM_SHAPES:
         d = make_inputs(4, M, K, N, group=GROUP, seed=0)
         p = packed_w4(d)
-        gemm.append(dict(M=M, K=K, N=N, A=upload(d["x"]), packed=p,
+        gemm.append(dict(M=M, K=K, N=N, A=upload(d["x"]), copies=[p] + [p.clone() for _ in range(GEMM_COPIES - 1)],
                          out=torch.empty((M, N), dtype=torch.float16, device=dev)))
         del d
     M1, K1, N1 = GEMV_SHAPE
@@ -402,46 +405,59 @@ def main():
     del d
     torch.cuda.synchronize()
 
-    def gemm_pair():
-        for g in gemm:
-            tf.w4a16_gemm(g["A"], g["packed"], g["K"], g["N"], GROUP, out=g["out"])
+    def gemm_one(g, c):
+        tf.w4a16_gemm(g["A"], g["copies"][c], g["K"], g["N"], GROUP, out=g["out"])
 
     def gemv_batch():
         for p in gemv_copies:
             tf.w4a16_gemv(x1, p, K1, N1, GROUP, out=y1)
 
-    # Warm-up runs eagerly (it also allocates the library's default
-    # workspace); then each half of the step is captured once as a HIP graph,
-    # so the timed launches follow each other on the GPU without host-side
-    # gaps (a Python call costs more than a decode GEMV runs).
-    for _ in range(max(1, args.warmup)):
-        gemm_pair()
-        gemv_batch()
+    # Each phase of the K timed steps is captured as ONE HIP
+    # graph: the K launches of a prefill shape, rotating over its weight
+    # copies, and the K decode GEMV batches.  Inside a graph the kernels
+    # follow each other on the GPU without gaps; each graph replay costs a
+    # launch gap of its own, which one replay per phase keeps out of the
+    # per-kernel figures.
+    gemm_one(gemm[0], 0)     # allocates the default workspace before capture
     torch.cuda.synchronize()
-    g_gemm, g_gemv = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g_gemm):
-        gemm_pair()
+    graphs = []
+    for g in gemm:
+        cg = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(cg):
+            for s in range(args.steps):
+                gemm_one(g, s % GEMM_COPIES)
+        graphs.append(cg)
+    g_gemv = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g_gemv):
-        gemv_batch()
+        for s in range(args.steps):
+            gemv_batch()
     torch.cuda.synchronize()
+    # The W warm-up steps run right before the timed region, so the GPU
+    # enters it busy (capture above leaves it idle, and clocks drop then).
+    for s in range(args.warmup):
+        for g in gemm:
+            gemm_one(g, s % GEMM_COPIES)
+        gemv_batch()
 
-    def step(ev):
-        ev[0].record(stream)
-        g_gemm.replay()
-        ev[1].record(stream)
-        g_gemv.replay()
-        ev[2].record(stream)
-
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    # The timed region holds the K steps' work grouped by kernel: the K
+    # launches of each prefill shape back to back (weights stream from HBM,
+    # the shape's activations stay cache-resident as the previous layer's
+    # output would), then the K decode GEMV batches.
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(graphs) + 2)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for s in range(args.steps):
-        step(events[s])
+    ev[0].record(stream)
+    for i, cg in enumerate(graphs):
+        cg.replay()
+        ev[i + 1].record(stream)
+    g_gemv.replay()
+    ev[-1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
-    gemm_ms = sum(e[0].elapsed_time(e[1]) for e in events) / args.steps
-    gemv_ms = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps
+    shape_ms = [ev[i].elapsed_time(ev[i + 1]) / args.steps for i in range(len(graphs))]
+    gemm_ms = sum(shape_ms)
+    gemv_ms = ev[-2].elapsed_time(ev[-1]) / args.steps
     gemm_flops = sum(2.0 * g["M"] * g["N"] * g["K"] for g in gemm)
     tflops = gemm_flops / (gemm_ms * 1e-3) / 1e12
     gemv_us = gemv_ms * 1e3 / GEMV_REPS
@@ -463,7 +479,8 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": "W4A16 (AWQ-style, G=128) prefill GEMM M=2048 at (K=4096,N=14336) and "
-                        "(K=14336,N=4096) + decode GEMV M=1 K=4096 N=14336 x%d weight copies" % GEMV_REPS,
+                        "(K=14336,N=4096) x%d weight copies + decode GEMV M=1 K=4096 N=14336 x%d "
+                        "weight copies" % (GEMM_COPIES, GEMV_REPS),
             "group": GROUP,
             "weights": "4-bit codes, fp16 scales, 4-bit zero-points (seeded uniform)",
             "activations": "fp16 N(0,1)",
@@ -489,6 +506,7 @@ def main():
                          "kernel": "gemv_kernel<4,1,16,4,2>"},
         },
         "gemm_ms_per_step": round(gemm_ms, 4),
+        "gemm_us_per_shape": {f"K={K},N={N}": round(t * 1e3, 2) for (M, K, N), t in zip(GEMM_SHAPES, shape_ms)},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline()
