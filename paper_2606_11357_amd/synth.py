@@ -33,6 +33,7 @@ __all__ = [
     "make_inputs",
     "make_inputs_w8sym",
     "WORKLOADS",
+    "make_inputs_bf16",
     "M_SWEEP",
     "M_SWEEP_SHAPES",
 ]
@@ -80,6 +81,47 @@ def make_inputs(bits: int, M: int, K: int, N: int, group: int = 128, seed: int =
     z = rng.integers(0, qmax + 1, size=(K // group, N), dtype=np.uint8)
     out = {"bits": bits, "M": M, "K": K, "N": N, "group": group,
            "x": x, "q": q, "s": s, "z": z}
+    if bits == 4:
+        out["qweight"] = pack_nibbles(q)
+        out["qzeros"] = pack_nibbles(z)
+    else:
+        out["qweight"] = q
+        out["zeros"] = z
+    return out
+
+
+def _bf16_bits(v: np.ndarray) -> np.ndarray:
+    """float32 draws -> bfloat16 bit patterns by keeping the high 16 bits
+    (truncation: the draw only has to be some bfloat16 value)."""
+    return (np.asarray(v, dtype=np.float32).view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def make_inputs_bf16(bits: int, M: int, K: int, N: int, group: int = 128, seed: int = 0,
+                     x_std: float = 1.0, s_lo: float | None = None, s_hi: float | None = None,
+                     ) -> dict:
+    """Draw one seeded workload with BF16 activations and scales.
+
+    Same draws and order as ``make_inputs`` (x -> q -> s -> z), except that x
+    and s are drawn in float32 and handed over as bfloat16 bit patterns
+    ``x_bits`` [M, K] and ``s_bits`` [K/G, N] (uint16).  The boundary tensors
+    are as in ``make_inputs``.
+    """
+    if bits not in (4, 8):
+        raise ValueError("bits must be 4 or 8")
+    if K % group != 0:
+        raise ValueError("K must be a multiple of the group size")
+    if bits == 4 and N % 8 != 0:
+        raise ValueError("W4 needs N a multiple of 8")
+    if s_lo is None:
+        s_lo, s_hi = (0.005, 0.02) if bits == 4 else (0.0003, 0.001)
+    qmax = (1 << bits) - 1
+    rng = np.random.default_rng(seed)
+    x = _bf16_bits((x_std * rng.standard_normal((M, K))).astype(np.float32))
+    q = rng.integers(0, qmax + 1, size=(K, N), dtype=np.uint8)
+    s = _bf16_bits(rng.uniform(s_lo, s_hi, size=(K // group, N)).astype(np.float32))
+    z = rng.integers(0, qmax + 1, size=(K // group, N), dtype=np.uint8)
+    out = {"bits": bits, "M": M, "K": K, "N": N, "group": group,
+           "x_bits": x, "q": q, "s_bits": s, "z": z}
     if bits == 4:
         out["qweight"] = pack_nibbles(q)
         out["qzeros"] = pack_nibbles(z)
