@@ -54,7 +54,7 @@ enum tf_status {
 };
 
 /* Output dtypes of tf_dequant. */
-enum tf_dtype { TF_F16 = 1, TF_F32 = 2 };
+enum tf_dtype { TF_F16 = 1, TF_F32 = 2, TF_BF16 = 3 };
 
 /* Largest accepted K and N (each) and M; keeps every byte offset in int64
  * and every per-kernel index in 32 bits. */
@@ -166,11 +166,40 @@ int tf_w8a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,
                   void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * BF16 activations and scales (the paper's dtype: Section 2.2 takes BF16
+ * activations, Section 4.2 stores BF16 scales beside each weight tile,
+ * Section 4.3 holds the dequantized weights in BF16 before the multiply):
+ *   C_bf16[M, N] = A_bf16[M, K] x RNE_bf16(s_bf16 * (q - z))[K, N],
+ * fp32 accumulate, C rounded to bfloat16, nearest even.
+ * The packed buffer is the same format: tf_pack_w4 / tf_pack_w8 /
+ * tf_pack_w8_sym copy the 16-bit scale patterns verbatim, so packing with
+ * bfloat16 scale bits gives a buffer for these entry points (and packing
+ * with fp16 bits one for the entry points above; the buffer does not record
+ * which).  Same shapes, alignment, workspace contract and tf_workspace_bytes
+ * as the fp16 entry points; the same kernels are chosen for each M.
+ * s * (q - z) is formed exactly in fp32 and rounded once to bfloat16.
+ */
+int tf_w4a16_gemm_bf16(const uint16_t* A_bf16, const void* packed, uint16_t* C_bf16,
+                       int64_t M, int64_t K, int64_t N, int group,
+                       void* workspace, size_t workspace_bytes, void* stream);
+int tf_w8a16_gemm_bf16(const uint16_t* A_bf16, const void* packed, uint16_t* C_bf16,
+                       int64_t M, int64_t K, int64_t N, int group,
+                       void* workspace, size_t workspace_bytes, void* stream);
+int tf_w4a16_gemv_bf16(const uint16_t* A_bf16, const void* packed, uint16_t* C_bf16,
+                       int64_t M, int64_t K, int64_t N, int group,
+                       void* workspace, size_t workspace_bytes, void* stream);
+int tf_w8a16_gemv_bf16(const uint16_t* A_bf16, const void* packed, uint16_t* C_bf16,
+                       int64_t M, int64_t K, int64_t N, int group,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Debug / test exports.  They read the packed buffer through the same device
  * unpack and dequantize code as the matmul kernels.
  *   tf_unpack : q_out uint8 [K, N] and z_out uint8 [K/G, N] (Section 4.3 unpack)
  *   tf_dequant: W_out [K, N] of s * (q - z) (Eq. 2), dtype TF_F16 (rounded
- *               once, nearest even) or TF_F32 (exact).
+ *               once, nearest even) or TF_F32 (exact), both reading the
+ *               scales as fp16; or TF_BF16: scales read as bfloat16, the
+ *               weight rounded once to bfloat16 as the BF16 entry points do.
  */
 int tf_unpack(int bits, const void* packed, int64_t K, int64_t N, int group,
               uint8_t* q_out, uint8_t* z_out, void* stream);

@@ -47,27 +47,27 @@ int check_workspace(const Layout& L, int64_t M, const void* ws, size_t ws_bytes)
 }
 
 int gemm_entry(int bits, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
-               int64_t K, int64_t N, int group, void* ws, size_t ws_bytes, void* stream) {
+               int64_t K, int64_t N, int group, void* ws, size_t ws_bytes, void* stream, bool bf) {
     int rc = check_matmul(bits, A, packed, C, M, K, N, group);
     if (rc) return rc;
     Layout L = tf::make_layout(bits, K, N, group);
     rc = check_workspace(L, M, ws, ws_bytes);
     if (rc) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (M < tf::kSkinnyMinM) return tf::launch_gemv(L, A, packed, C, M, ws, s);
-    if (M <= tf::kSkinnyMaxM) return tf::launch_skinny_gemm(L, A, packed, C, M, ws, s);
-    return tf::launch_gemm(L, A, packed, C, M, ws, ws_bytes, s);
+    if (M < tf::kSkinnyMinM) return tf::launch_gemv(L, A, packed, C, M, ws, s, bf);
+    if (M <= tf::kSkinnyMaxM) return tf::launch_skinny_gemm(L, A, packed, C, M, ws, s, bf);
+    return tf::launch_gemm(L, A, packed, C, M, ws, ws_bytes, s, bf);
 }
 
 int gemv_entry(int bits, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
-               int64_t K, int64_t N, int group, void* ws, size_t ws_bytes, void* stream) {
+               int64_t K, int64_t N, int group, void* ws, size_t ws_bytes, void* stream, bool bf) {
     int rc = check_matmul(bits, A, packed, C, M, K, N, group);
     if (rc) return rc;
     if (M > TF_GEMV_MAX_M) return TF_ERR_ARG;
     Layout L = tf::make_layout(bits, K, N, group);
     rc = check_workspace(L, M, ws, ws_bytes);
     if (rc) return rc;
-    return tf::launch_gemv(L, A, packed, C, M, ws, static_cast<hipStream_t>(stream));
+    return tf::launch_gemv(L, A, packed, C, M, ws, static_cast<hipStream_t>(stream), bf);
 }
 
 }  // namespace
@@ -137,25 +137,57 @@ int64_t tf_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group)
 int tf_w4a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
                   int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
                   void* stream) {
-    return gemm_entry(4, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream);
+    return gemm_entry(4, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream,
+                      false);
+}
+
+int tf_w4a16_gemm_bf16(const uint16_t* A_bf16, const void* packed, uint16_t* C_bf16, int64_t M,
+                       int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    return gemm_entry(4, A_bf16, packed, C_bf16, M, K, N, group, workspace, workspace_bytes, stream,
+                      true);
 }
 
 int tf_w8a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
                   int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
                   void* stream) {
-    return gemm_entry(8, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream);
+    return gemm_entry(8, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream,
+                      false);
+}
+
+int tf_w8a16_gemm_bf16(const uint16_t* A_bf16, const void* packed, uint16_t* C_bf16, int64_t M,
+                       int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    return gemm_entry(8, A_bf16, packed, C_bf16, M, K, N, group, workspace, workspace_bytes, stream,
+                      true);
 }
 
 int tf_w4a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
                   int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
                   void* stream) {
-    return gemv_entry(4, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream);
+    return gemv_entry(4, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream,
+                      false);
+}
+
+int tf_w4a16_gemv_bf16(const uint16_t* A_bf16, const void* packed, uint16_t* C_bf16, int64_t M,
+                       int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    return gemv_entry(4, A_bf16, packed, C_bf16, M, K, N, group, workspace, workspace_bytes, stream,
+                      true);
 }
 
 int tf_w8a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
                   int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
                   void* stream) {
-    return gemv_entry(8, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream);
+    return gemv_entry(8, A_f16, packed, C_f16, M, K, N, group, workspace, workspace_bytes, stream,
+                      false);
+}
+
+int tf_w8a16_gemv_bf16(const uint16_t* A_bf16, const void* packed, uint16_t* C_bf16, int64_t M,
+                       int64_t K, int64_t N, int group, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    return gemv_entry(8, A_bf16, packed, C_bf16, M, K, N, group, workspace, workspace_bytes, stream,
+                      true);
 }
 
 int tf_unpack(int bits, const void* packed, int64_t K, int64_t N, int group, uint8_t* q_out,
@@ -173,7 +205,7 @@ int tf_dequant(int bits, const void* packed, int64_t K, int64_t N, int group, in
     if (!packed || !W_out) return TF_ERR_NULL;
     int rc = check_weight(bits, K, N, group);
     if (rc) return rc;
-    if (out_dtype != TF_F16 && out_dtype != TF_F32) return TF_ERR_ARG;
+    if (out_dtype != TF_F16 && out_dtype != TF_F32 && out_dtype != TF_BF16) return TF_ERR_ARG;
     if (misaligned(packed) || misaligned(W_out)) return TF_ERR_ALIGN;
     return tf::launch_dequant(tf::make_layout(bits, K, N, group), packed, out_dtype, W_out,
                               static_cast<hipStream_t>(stream));

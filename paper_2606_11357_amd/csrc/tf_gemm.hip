@@ -59,7 +59,7 @@ struct SplitK {
     float* part;
 };
 
-template <int BITS, int MPC>
+template <int BITS, int MPC, bool BF>
 __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
     int M, int K, int N, int gshift, int64_t s_off, int64_t z_off, int na, int ng, int np,
@@ -173,33 +173,37 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
             }
         }
     };
-    // Group constants: (s, s), -(1024 + z), -(64 + z) for each lane column.
+    // Group constants of each lane column (see DqConst).
     struct Consts {
-        half2_t s2[4];
-        uint32_t nz[4], nz64[4];
+        DqConst<BF> q[4];
     };
     auto make_consts = [&](const Meta& mt, int m, Consts& k) {
 #pragma unroll
         for (int pp = 0; pp < PANELS; ++pp)
 #pragma unroll
             for (int t = 0; t < T; ++t) {
-                const uint32_t sh = mt.s[m][pp][t / 2] >> (16 * (t & 1));
-                k.s2[pp * T + t] = as_h2(__builtin_amdgcn_perm(sh, sh, 0x01000100u));
-                const uint32_t n = __builtin_amdgcn_perm(0xE4E4E4E4u, mt.z[m][pp], 0x04000400u | (t * 0x00010001u));
-                k.nz[pp * T + t] = n;
-                k.nz64[pp * T + t] = neg_zero64_pair(n);
+                DqConst<BF>& kq = k.q[pp * T + t];
+                if constexpr (BF) {
+                    const uint32_t sw = mt.s[m][pp][t / 2];
+                    kq.s = __builtin_bit_cast(float, (t & 1) ? (sw & 0xFFFF0000u) : (sw << 16));
+                    kq.nzs = -(byte_f32(mt.z[m][pp], t) * kq.s);
+                } else {
+                    const uint32_t sh = mt.s[m][pp][t / 2] >> (16 * (t & 1));
+                    kq.s2 = as_h2(__builtin_amdgcn_perm(sh, sh, 0x01000100u));
+                    const uint32_t n = __builtin_amdgcn_perm(0xE4E4E4E4u, mt.z[m][pp], 0x04000400u | (t * 0x00010001u));
+                    kq.nz = n;
+                    kq.nz64 = neg_zero64_pair(n);
+                }
             }
     };
-    auto dequant = [&](const u32x4 (&slot)[PANELS], const Consts& k, half8_t (&bop)[4]) {
+    auto dequant = [&](const u32x4 (&slot)[PANELS], const Consts& k, u32x4 (&bop)[4]) {
 #pragma unroll
         for (int pp = 0; pp < PANELS; ++pp)
 #pragma unroll
             for (int t = 0; t < T; ++t) {
                 const int u = pp * T + t;
-                if constexpr (BITS == 4)
-                    bop[u] = dq_w4_dword(slot[pp][t], magic, k.nz[u], k.nz64[u], k.s2[u]);
-                else
-                    bop[u] = dq_w8_dwords(slot[pp][2 * t], slot[pp][2 * t + 1], k.nz[u], k.s2[u]);
+                bop[u] = dq_operand<BF, BITS>(slot[pp][BITS == 4 ? t : 2 * t],
+                                              slot[pp][BITS == 4 ? t : 2 * t + 1], magic, k.q[u]);
             }
     };
 
@@ -217,7 +221,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
     store_a(0, ra[0]);
     Consts kc;
     make_consts(mcur, 0, kc);
-    half8_t bop[4];
+    u32x4 bop[4];
     dequant(ring[0], kc, bop);
 
     for (int ch = 0; ch < chunks; ++ch) {
@@ -237,15 +241,14 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
                 make_consts(mcur, (j + 1) / SPG, kc);     // next step starts a new group
             }
             __syncthreads();                              // As[buf] written; As[(step + 1) % 3] free
-            half8_t bnext[4];
+            u32x4 bnext[4];
             dequant(ring[(j + 1) % CS], kc, bnext);       // B operands of step + 1
             if (live) {
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
-                    const half8_t af = __builtin_bit_cast(half8_t, As[buf][a_slot(16 * i + c, kg)]);
+                    const u32x4 af = As[buf][a_slot(16 * i + c, kg)];
 #pragma unroll
-                    for (int t = 0; t < 4; ++t)
-                        acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bop[t], acc[i][t], 0, 0, 0);
+                    for (int t = 0; t < 4; ++t) acc[i][t] = mfma16<BF>(af, bop[t], acc[i][t]);
                 }
             }
 #pragma unroll
@@ -260,7 +263,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int64_t row = row0 + 16 * i + 4 * kg + r;
-            if (row < M && col < N) C[row * N + col] = __builtin_bit_cast(uint16_t, (_Float16)v[r]);
+            if (row < M && col < N) C[row * N + col] = round_out<BF>(v[r]);
         }
     };
     if (sk.S == 1) {
@@ -330,7 +333,7 @@ constexpr int kBM1 = 128, kBN1 = 128, kBK1 = 32;
 
 __device__ __forceinline__ int a_swz1(int row, int chunk) { return row * 4 + (chunk ^ ((row >> 2) & 3)); }
 
-template <int BITS>
+template <int BITS, bool BF>
 __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_generic(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
     int M, int K, int N, int group, int64_t s_off, int64_t z_off, int na, int ng, int np) {
@@ -365,7 +368,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_generic(
             av[r] = grow < M ? *reinterpret_cast<const u32x4*>(A + grow * K + (int64_t)a * kBK1 + ch * 8)
                              : u32x4{0u, 0u, 0u, 0u};
         }
-        half8_t b[4];
+        u32x4 b[4];
         const int g = (a * kBK1) / group;
 #pragma unroll
         for (int pp = 0; pp < kPanels; ++pp) {
@@ -389,12 +392,11 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_generic(
             }
 #pragma unroll
             for (int t = 0; t < T; ++t) {
-                const half2_t s2 = as_h2((uint32_t)sb[t] | ((uint32_t)sb[t] << 16));
-                const uint32_t nz = neg_zero_pair(zb[t]);
+                const DqConst<BF> kq = make_dq_const<BF>(sb[t], zb[t]);
                 if constexpr (BITS == 4)
-                    b[t] = dq_w4_dword(wv[t], magic, nz, neg_zero64_pair(nz), s2);
+                    b[t] = dq_operand<BF, 4>(wv[t], 0u, magic, kq);
                 else
-                    b[pp * T + t] = dq_w8_dwords(wv[2 * t], wv[2 * t + 1], nz, s2);
+                    b[pp * T + t] = dq_operand<BF, 8>(wv[2 * t], wv[2 * t + 1], magic, kq);
             }
         }
         __syncthreads();
@@ -406,10 +408,9 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_generic(
         __syncthreads();
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const half8_t af = __builtin_bit_cast(half8_t, As[a_swz1(wm * 64 + 16 * i + c, kg)]);
+            const u32x4 af = As[a_swz1(wm * 64 + 16 * i + c, kg)];
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
-                acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, b[t], acc[i][t], 0, 0, 0);
+            for (int t = 0; t < 4; ++t) acc[i][t] = mfma16<BF>(af, b[t], acc[i][t]);
         }
     }
 
@@ -422,7 +423,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_generic(
             for (int r = 0; r < 4; ++r) {
                 const int64_t row = row0 + wm * 64 + 16 * i + 4 * kg + r;
                 if (row < M && col < N)
-                    C[row * N + col] = __builtin_bit_cast(uint16_t, (_Float16)acc[i][t][r]);
+                    C[row * N + col] = round_out<BF>(acc[i][t][r]);
             }
         }
 }
@@ -463,7 +464,7 @@ bool main_kernel_fits(const Layout& L, int bits) {
     return L.K % chunk_rows == 0 && (L.group & (L.group - 1)) == 0 && bits > 0;
 }
 
-template <int BITS, int MPC>
+template <int BITS, int MPC, bool BF>
 int launch_main(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
                 void* ws, hipStream_t s) {
     const int tiles_m = (int)((M + kBM - 1) / kBM);
@@ -476,12 +477,12 @@ int launch_main(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t*
         sk.cnt = static_cast<uint32_t*>(ws);
         sk.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes);
     }
-    return launch(gemm_kernel<BITS, MPC>, dim3((unsigned)(tiles_m * tiles_n * sp.S)), dim3(kGemmThreads),
+    return launch(gemm_kernel<BITS, MPC, BF>, dim3((unsigned)(tiles_m * tiles_n * sp.S)), dim3(kGemmThreads),
                   0, s, A, pk, C, (int)M, (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na,
                   (int)L.ng, (int)L.np, tiles_m, tiles_n, sk);
 }
 
-template <int BITS>
+template <int BITS, bool BF>
 int launch_bits(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
                 void* ws, hipStream_t s) {
     constexpr int CS = chunk_steps<BITS>();
@@ -489,12 +490,12 @@ int launch_bits(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t*
     const bool pow2_group = (L.group & (L.group - 1)) == 0;
     if (L.K % chunk_rows == 0 && pow2_group) {
         const int mpc = L.group >= chunk_rows ? 1 : chunk_rows / L.group;
-        if (mpc == 1) return launch_main<BITS, 1>(L, A, pk, C, M, ws, s);
-        if (mpc == 2) return launch_main<BITS, 2>(L, A, pk, C, M, ws, s);
-        if constexpr (CS >= 4) return launch_main<BITS, 4>(L, A, pk, C, M, ws, s);
+        if (mpc == 1) return launch_main<BITS, 1, BF>(L, A, pk, C, M, ws, s);
+        if (mpc == 2) return launch_main<BITS, 2, BF>(L, A, pk, C, M, ws, s);
+        if constexpr (CS >= 4) return launch_main<BITS, 4, BF>(L, A, pk, C, M, ws, s);
     }
     dim3 grid((unsigned)((L.N + kBN1 - 1) / kBN1), (unsigned)((M + kBM1 - 1) / kBM1));
-    return launch(gemm_kernel_generic<BITS>, grid, dim3(kGemmThreads), 0, s, A, pk, C, (int)M,
+    return launch(gemm_kernel_generic<BITS, BF>, grid, dim3(kGemmThreads), 0, s, A, pk, C, (int)M,
                   (int)L.K, (int)L.N, L.group, L.s_off, L.z_off, (int)L.na, (int)L.ng, (int)L.np);
 }
 
@@ -518,13 +519,17 @@ int64_t gemm_workspace_bytes(const Layout& L, int64_t M) {
 }
 
 int launch_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
-                void* ws, size_t ws_bytes, hipStream_t s) {
+                void* ws, size_t ws_bytes, hipStream_t s, bool bf) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    if (use_gemm256(L, M, ws)) return launch_gemm256(L, A, pk, C, M, ws, ws_bytes, s);
+    if (use_gemm256(L, M, ws)) return launch_gemm256(L, A, pk, C, M, ws, ws_bytes, s, bf);
     // a workspace too small for this kernel's split (sized for another
     // kernel of a larger M) selects the single-pass form
     if (ws && (int64_t)ws_bytes < gemm_workspace_bytes(L, M)) ws = nullptr;
-    return L.bits == 4 ? launch_bits<4>(L, A, pk, C, M, ws, s) : launch_bits<8>(L, A, pk, C, M, ws, s);
+    if (bf)
+        return L.bits == 4 ? launch_bits<4, true>(L, A, pk, C, M, ws, s)
+                           : launch_bits<8, true>(L, A, pk, C, M, ws, s);
+    return L.bits == 4 ? launch_bits<4, false>(L, A, pk, C, M, ws, s)
+                       : launch_bits<8, false>(L, A, pk, C, M, ws, s);
 }
 
 }  // namespace tf

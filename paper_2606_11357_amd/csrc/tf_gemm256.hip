@@ -48,8 +48,12 @@ __device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff,
 // Written as an asm statement because the register allocator otherwise
 // moves the 256 loop-carried accumulators between AGPRs and VGPRs at every
 // step; the asm is not volatile, so it still schedules freely.
-__device__ __forceinline__ void mfma_acc(float4_t& acc, const half8_t& a, const half8_t& b) {
-    asm("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+template <bool BF>
+__device__ __forceinline__ void mfma_acc(float4_t& acc, const u32x4& a, const u32x4& b) {
+    if constexpr (BF)
+        asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+    else
+        asm("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
 // The weights go in as the first operand and the activations as the second,
 // so each accumulator block is a 16 (n) x 16 (m) tile of C transposed: lane l
@@ -110,7 +114,17 @@ __device__ __forceinline__ int sk_owner(int64_t u, int G, int U) {   // block wh
 }
 __device__ __forceinline__ int sk_begin(int v, int G, int U) { return (int)((int64_t)v * U / G); }
 
-template <int BITS, int MPC>
+// Slots of a K step's 64 that carry dequantization micro-steps: 4 .. 63.
+// fp16 needs at most 52 micro-steps per step (one per slot from slot 4);
+// bf16 needs 88 (4-bit) or 80 (8-bit), spread one or two per slot.
+constexpr int kDqFirstSlot = 4, kDqSlots = 64 - kDqFirstSlot;
+// first micro-step of slot q (q = kDqFirstSlot .. 64) when R are placed
+constexpr int dq_slot_begin(int q, int R) {
+    return R <= kDqSlots ? (q - kDqFirstSlot < R ? q - kDqFirstSlot : R)
+                         : (q - kDqFirstSlot) * R / kDqSlots;
+}
+
+template <int BITS, int MPC, bool BF>
 __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
     int M, int K, int N, int gshift, int64_t s_off, int64_t z_off, int na, int ng, int np,
@@ -132,7 +146,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     const uint32_t magic = magic_reg();
     const int steps = na;
     const int chunks = steps / kCS;            // the launcher requires K % 128 == 0
-    constexpr int kDqSteps = BITS == 4 ? kDqW4Steps : kDqW8Steps;
+    constexpr int kDqSteps = dq_steps<BF, BITS>();
+    constexpr int kDqTotal = 4 * kDqSteps;     // micro-steps per K step
+    static_assert(kDqTotal <= 2 * kDqSlots, "at most two micro-steps per slot");
 
     // A step tile (256 rows x 32 halves = 1024 16-byte slots) arrives by four
     // direct loads per thread; load r of wave w fills slots (4 w + r) * 64 +
@@ -146,45 +162,47 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         const int row = x >> 2, chk = (x & 3) ^ ((row >> 2) & 3);
         avoff[r] = (uint32_t)row * (uint32_t)K * 2u + (uint32_t)chk * 16u;
     }
-    auto read_a = [&](int buf, int i) {
-        return __builtin_bit_cast(half8_t, abuf(buf)[a_slot(16 * i + c, kg)]);
-    };
+    auto read_a = [&](int buf, int i) { return abuf(buf)[a_slot(16 * i + c, kg)]; };
     struct Meta {
         uint32_t s[MPC][PANELS][(T + 1) / 2];   // T fp16 scales per group and panel
         uint32_t z[MPC][PANELS];                // T zero-point bytes
     };
-    // Group constants per lane column: (s, s), -(1024 + z), -(64 + z).
+    // Group constants of each lane column (see DqConst).
     struct Consts {
-        half2_t s2[4];
-        uint32_t nz[4], nz64[4];
+        DqConst<BF> q[4];
     };
     auto make_consts = [&](const Meta& mt, int m, Consts& k) {
 #pragma unroll
         for (int pp = 0; pp < PANELS; ++pp)
 #pragma unroll
             for (int t = 0; t < T; ++t) {
-                const uint32_t sh = mt.s[m][pp][t / 2] >> (16 * (t & 1));
-                k.s2[pp * T + t] = as_h2(__builtin_amdgcn_perm(sh, sh, 0x01000100u));
-                const uint32_t n = __builtin_amdgcn_perm(0xE4E4E4E4u, mt.z[m][pp], 0x04000400u | (t * 0x00010001u));
-                k.nz[pp * T + t] = n;
-                k.nz64[pp * T + t] = neg_zero64_pair(n);
+                DqConst<BF>& kq = k.q[pp * T + t];
+                if constexpr (BF) {
+                    const uint32_t sw = mt.s[m][pp][t / 2];
+                    kq.s = __builtin_bit_cast(float, (t & 1) ? (sw & 0xFFFF0000u) : (sw << 16));
+                    kq.nzs = -(byte_f32(mt.z[m][pp], t) * kq.s);
+                } else {
+                    const uint32_t sh = mt.s[m][pp][t / 2] >> (16 * (t & 1));
+                    kq.s2 = as_h2(__builtin_amdgcn_perm(sh, sh, 0x01000100u));
+                    const uint32_t n = __builtin_amdgcn_perm(0xE4E4E4E4u, mt.z[m][pp], 0x04000400u | (t * 0x00010001u));
+                    kq.nz = n;
+                    kq.nz64 = neg_zero64_pair(n);
+                }
             }
     };
     // Dequantization micro-step k of B operand u (0..3) from ring slot `slot`.
-    auto dq_step = [&](int u, int k, const u32x4 (&slot)[PANELS], const Consts& kk, DqState& st) {
+    auto dq_step_u = [&](int u, int k, const u32x4 (&slot)[PANELS], const Consts& kk, DqSt<BF>& st) {
         const int pp = u / T, t = u % T;
-        if constexpr (BITS == 4)
-            dq_w4_step(k, slot[pp][t], magic, kk.nz[u], kk.nz64[u], kk.s2[u], st);
-        else
-            dq_w8_step(k, slot[pp][2 * t], slot[pp][2 * t + 1], kk.nz[u], kk.s2[u], st);
+        dq_step<BF, BITS>(k, slot[pp][BITS == 4 ? t : 2 * t], slot[pp][BITS == 4 ? t : 2 * t + 1], magic,
+                          kk.q[u], st);
     };
-    auto dequant = [&](const u32x4 (&slot)[PANELS], const Consts& kk, half8_t (&bop)[4]) {
+    auto dequant = [&](const u32x4 (&slot)[PANELS], const Consts& kk, u32x4 (&bop)[4]) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            DqState st;
+            DqSt<BF> st;
 #pragma unroll
-            for (int k = 0; k < kDqSteps; ++k) dq_step(u, k, slot, kk, st);
-            bop[u] = __builtin_bit_cast(half8_t, st.out);
+            for (int k = 0; k < kDqSteps; ++k) dq_step_u(u, k, slot, kk, st);
+            bop[u] = st.out;
         }
     };
 
@@ -208,9 +226,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const float4_t a = blk[t];
-                const half2_t lo = {(_Float16)a[0], (_Float16)a[1]};
-                const half2_t hi = {(_Float16)a[2], (_Float16)a[3]};
-                *reinterpret_cast<uint2*>(stage + c * kStageRow + 32 * t + 8 * kg) = uint2{as_u32(lo), as_u32(hi)};
+                *reinterpret_cast<uint2*>(stage + c * kStageRow + 32 * t + 8 * kg) =
+                    uint2{round_out2<BF>(a[0], a[1]), round_out2<BF>(a[2], a[3])};
             }
             __builtin_amdgcn_s_waitcnt(0xC07F);       // lgkmcnt(0): this wave's stores landed
             u32x4 v[2];
@@ -311,7 +328,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         load_meta(c0 + 1, mnext);
         Consts kc;
         make_consts(mcur, 0, kc);
-        half8_t bop[4];
+        u32x4 bop[4];
         dequant(ring[0], kc, bop);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
@@ -319,7 +336,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         // per step, so the pattern repeats exactly from step to step); reads
         // run four blocks ahead.
         constexpr int kLead = 4, kRing = 8;
-        half8_t af[kRing];
+        u32x4 af[kRing];
 #pragma unroll
         for (int i = 0; i < kLead; ++i) af[i] = read_a(0, i);
         mfma_hazard_gap();
@@ -336,9 +353,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         //                 ring, so each LDS read has four blocks to land); for
         //                 i = 12..15 fragment i - 12 of step s+1 instead
         //                 (written before the previous barrier)
-        //   slots 4..55   the 52 (4-bit) or 48 (8-bit) dequantization
-        //                 micro-steps of step s+1's B operands, one vector
-        //                 instruction each, issued while the matrix core works
+        //   slots 4..     the dequantization micro-steps of step s+1's B
+        //                 operands, one vector instruction each, issued while
+        //                 the matrix core works: fp16 52 (4-bit) or 48 (8-bit),
+        //                 one per slot from slot 4; bf16 88 or 80, one or two
+        //                 per slot over slots 4..63
         // then one barrier, after this wave's direct loads of step s+2 (issued
         // during step s-1) have landed.
         for (int ch = c0; ch < c1; ++ch) {
@@ -353,22 +372,25 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                 } else if ((j + 1) % SPG == 0) {
                     make_consts(mcur, (j + 1) / SPG, kc); // next step starts a new group
                 }
-                half8_t bnext[4];
-                DqState st[4];
+                u32x4 bnext[4];
+                DqSt<BF> st[4];
 #pragma unroll
                 for (int q = 0; q < 4 * kRB; ++q) {
                     const int i = q / 4, t = q % 4;
                     __builtin_amdgcn_sched_barrier(0);
-                    mfma_acc(acc[i][t], bop[t], af[i % kRing]);
+                    mfma_acc<BF>(acc[i][t], bop[t], af[i % kRing]);
                     if (q == 0) load_atom(step + 4, ring[j]);
                     if (q % 4 == 2 && q < 16) dma_a(step + 3, (j + 3) % kABufs, q / 4);
                     if (t == 0 && i + kLead < kRB) af[(i + kLead) % kRing] = read_a(buf, i + kLead);
                     if (t == 0 && i + kLead >= kRB)
                         af[i + kLead - kRB] = read_a((j + 1) % kABufs, i + kLead - kRB);
-                    if (q >= 4 && q < 4 + 4 * kDqSteps) {
-                        const int o = q - 4, u = o / kDqSteps, k = o % kDqSteps;
-                        dq_step(u, k, ring[(j + 1) % kCS], kc, st[u]);
-                        if (k == kDqSteps - 1) bnext[u] = __builtin_bit_cast(half8_t, st[u].out);
+                    if (q >= kDqFirstSlot) {
+#pragma unroll
+                        for (int o = dq_slot_begin(q, kDqTotal); o < dq_slot_begin(q + 1, kDqTotal); ++o) {
+                            const int u = o / kDqSteps, k = o % kDqSteps;
+                            dq_step_u(u, k, ring[(j + 1) % kCS], kc, st[u]);
+                            if (k == kDqSteps - 1) bnext[u] = st[u].out;
+                        }
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -506,7 +528,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     }
 }
 
-template <int BITS, int MPC>
+template <int BITS, int MPC, bool BF>
 int launch_mpc(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
                StreamK sk, int tiles_m, int tiles_n, hipStream_t s) {
     const int gshift = __builtin_ctz((unsigned)L.group);
@@ -515,7 +537,7 @@ int launch_mpc(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* 
     const int64_t a_bytes = M * L.K * 2, w_bytes = L.total;
     const int col_major = w_bytes > a_bytes ? 1 : 0;
     const unsigned grid = sk.groups ? (unsigned)sk.groups : (unsigned)(tiles_m * tiles_n);
-    return launch(gemm256_kernel<BITS, MPC>, dim3(grid), dim3(kThreads), 0, s, A, pk, C, (int)M,
+    return launch(gemm256_kernel<BITS, MPC, BF>, dim3(grid), dim3(kThreads), 0, s, A, pk, C, (int)M,
                   (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na, (int)L.ng, (int)L.np,
                   tiles_m, tiles_n, col_major, sk);
 }
@@ -550,8 +572,26 @@ int64_t gemm256_workspace_bytes(const Layout& L, int64_t M) {
     return kWsCounterBytes + (int64_t)2 * kSkMaxGroups * kBM * kBN * 4;
 }
 
+namespace {
+template <bool BF>
+int launch_bf(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
+              StreamK sk, int tiles_m, int tiles_n, hipStream_t s) {
+    const int chunk_rows = kBK * kCS;
+    const int mpc = L.group >= chunk_rows ? 1 : chunk_rows / L.group;
+    if (L.bits == 4) {
+        if (mpc == 1) return launch_mpc<4, 1, BF>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+        if (mpc == 2) return launch_mpc<4, 2, BF>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+        return launch_mpc<4, 4, BF>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+    }
+    if (mpc == 1) return launch_mpc<8, 1, BF>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+    if (mpc == 2) return launch_mpc<8, 2, BF>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+    return launch_mpc<8, 4, BF>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+}
+
+}  // namespace
+
 int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
-                   void* ws, size_t ws_bytes, hipStream_t s) {
+                   void* ws, size_t ws_bytes, hipStream_t s, bool bf) {
     const int tiles_m = (int)((M + kBM - 1) / kBM);
     const int tiles_n = (int)((L.N + kBN - 1) / kBN);
     const int tiles = tiles_m * tiles_n, chunks = (int)(L.K / (kBK * kCS));
@@ -585,16 +625,8 @@ int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16
         sk = StreamK{G, (int)units, static_cast<uint32_t*>(ws),
                      reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes), dp_rounds};
     }
-    const int chunk_rows = kBK * kCS;
-    const int mpc = L.group >= chunk_rows ? 1 : chunk_rows / L.group;
-    if (L.bits == 4) {
-        if (mpc == 1) return launch_mpc<4, 1>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
-        if (mpc == 2) return launch_mpc<4, 2>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
-        return launch_mpc<4, 4>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
-    }
-    if (mpc == 1) return launch_mpc<8, 1>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
-    if (mpc == 2) return launch_mpc<8, 2>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
-    return launch_mpc<8, 4>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+    return bf ? launch_bf<true>(L, A, pk, C, M, sk, tiles_m, tiles_n, s)
+              : launch_bf<false>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
 }
 
 bool gemm256_fills_device(const Layout& L, int64_t M) {

@@ -74,7 +74,7 @@ struct WaveStage {
 // SEG > 0: segments (atoms summed before the scale is applied) have SEG
 // atoms, fixed at compile time (one group of 32 SEG rows); SEG = 0: group
 // size known at run time.  D: weight atoms a wave keeps in flight.
-template <int BITS, int M, int WAVES, int SEG, int D>
+template <int BITS, int M, int WAVES, int SEG, int D, bool BF>
 __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
     int K, int N, int group, int64_t s_off, int64_t z_off, int na, int ng, int S, int AS, int RW,
@@ -106,7 +106,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar) index math
     const int c = lane & 15, kg = lane >> 4;
     const int apg = group / kAtomK;
-    const uint32_t magic = magic_reg();
+    const uint32_t magic = BF ? magic_bf_reg() : magic_reg();
     const uint32_t magic64 = magic64_reg();
     // this wave's run: atoms aw0 .. aw_end-1 of the panel (RW per wave; a
     // multiple of the group's atoms when SEG > 0)
@@ -203,17 +203,18 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         st.z[min(lane, ZLANES - 1)] = mt.zr;
         if constexpr (FACT) {
             // Sums of x per 8-k slice, once for all columns: sx = sum x and
-            // B = sum x * offset (1024 for rows 0,1,4,5 and, 4-bit, 64 for
-            // rows 2,3,6,7).  Lane l holds rows 4(l%2)..+3 of slice l/2: its
-            // first pair has offset 1024, its second 1024 or 64.
-            const half2_t ones = {(_Float16)1.0f, (_Float16)1.0f};
-            const half2_t o_lo = {(_Float16)1024.0f, (_Float16)1024.0f};
-            const half2_t o_hi = BITS == 4 ? half2_t{(_Float16)64.0f, (_Float16)64.0f} : o_lo;
+            // B = sum x * offset.  fp16: offset 1024 for rows 0,1,4,5 and,
+            // 4-bit, 64 for rows 2,3,6,7 (lane l holds rows 4(l%2)..+3 of
+            // slice l/2: its first pair has offset 1024, its second 1024 or
+            // 64).  bf16: 128 for every 4-bit row, 0 for 8-bit codes.
+            const uint32_t ones = BF ? 0x3F803F80u : 0x3C003C00u;
+            const uint32_t o_lo = BF ? (BITS == 4 ? 0x43004300u : 0u) : 0x64006400u;
+            const uint32_t o_hi = BF ? o_lo : (BITS == 4 ? 0x54005400u : 0x64006400u);
 #pragma unroll
             for (int m = 0; m < M; ++m) {
                 const uint32_t x01 = (uint32_t)mt.xr[m], x23 = (uint32_t)(mt.xr[m] >> 32);
-                float sx = __builtin_amdgcn_fdot2(as_h2(x23), ones, __builtin_amdgcn_fdot2(as_h2(x01), ones, 0.f, false), false);
-                float bo = __builtin_amdgcn_fdot2(as_h2(x23), o_hi, __builtin_amdgcn_fdot2(as_h2(x01), o_lo, 0.f, false), false);
+                float sx = dot2<BF>(x23, ones, dot2<BF>(x01, ones, 0.f));
+                float bo = (BF && BITS == 8) ? 0.f : dot2<BF>(x23, o_hi, dot2<BF>(x01, o_lo, 0.f));
                 sx += __shfl_xor(sx, 1);
                 bo += __shfl_xor(bo, 1);
                 // both lanes of a slice store its sums (no branch: a masked
@@ -229,8 +230,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 
         float acc[M][T];                 // factored form: sums of x * code of the open segment
         float bo[M], sx[M];              // ... and the segment's sums of x * offset and of x
-        half2_t s2[T];                   // dequant form: the open segment's scale and zero-point
-        uint32_t nz[T], nz64[T];
+        DqConst<BF> kq[T];               // dequant form: the open segment's scale and zero-point
         auto open = [&]() {
             if constexpr (FACT) {
 #pragma unroll
@@ -244,12 +244,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                 const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
                 const uint8_t* zp = zbytes + gl * PW + c * T;
 #pragma unroll
-                for (int t = 0; t < T; ++t) {
-                    const uint32_t sb = sp[t];
-                    s2[t] = as_h2(sb | (sb << 16));
-                    nz[t] = neg_zero_pair(zp[t]);
-                    if constexpr (BITS == 4) nz64[t] = neg_zero64_pair(nz[t]);
-                }
+                for (int t = 0; t < T; ++t) kq[t] = make_dq_const<BF>(sp[t], zp[t]);
             }
         };
         // close the open segment: y += s * (acc - bo - z * sx)
@@ -260,7 +255,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 #pragma unroll
                 for (int t = 0; t < T; ++t) {
                     const float zf = (float)zp[t];
-                    const float sf = (float)__builtin_bit_cast(_Float16, sp[t]);
+                    const float sf = scale_f32<BF>(sp[t]);
 #pragma unroll
                     for (int m = 0; m < M; ++m)
                         y[m][t] = fmaf(sf, acc[m][t] - fmaf(zf, sx[m], bo[m]), y[m][t]);
@@ -305,24 +300,32 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
             for (int t = 0; t < T; ++t) {
                 uint32_t P[4];
                 if constexpr (FACT) {
-                    if constexpr (BITS == 4) {
+                    if constexpr (BF && BITS == 4) {
+                        w4_code_pairs(wd[t], magic, P);          // rows (2q, 2q+1) as 128 + q
+                    } else if constexpr (BF) {
+                        // bytes have 8 bits, past bfloat16's exact 128 + v range:
+                        // each code converts to fp32 and back, exactly
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const uint32_t wq = wd[2 * t + q / 2];
+                            const bf16x2_t v = {(__bf16)byte_f32(wq, 2 * (q & 1)), (__bf16)byte_f32(wq, 2 * (q & 1) + 1)};
+                            P[q] = __builtin_bit_cast(uint32_t, v);
+                        }
+                    } else if constexpr (BITS == 4) {
                         w4_code_pairs_sum(wd[t], magic, magic64, P);
                     } else {
                         w8_code_pairs(wd[2 * t], P);
                         w8_code_pairs(wd[2 * t + 1], P + 2);
                     }
                 } else {
-                    const half8_t w8 = BITS == 4 ? dq_w4_dword(wd[t], magic, nz[t], nz64[t], s2[t])
-                                                 : dq_w8_dwords(wd[2 * t], wd[2 * t + 1], nz[t], s2[t]);
+                    const u32x4 wu = dq_operand<BF, BITS>(wd[BITS == 4 ? t : 2 * t], wd[BITS == 4 ? t : 2 * t + 1],
+                                                          magic, kq[t]);
                     if constexpr (MF) {
                         // the dequantized dword is the B operand of columns c + 16 t
 #pragma unroll
-                        for (int b = 0; b < MB; ++b)
-                            macc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                                __builtin_bit_cast(half8_t, afrag[b]), w8, macc[b][t], 0, 0, 0);
+                        for (int b = 0; b < MB; ++b) macc[b][t] = mfma16<BF>(afrag[b], wu, macc[b][t]);
                         continue;
                     }
-                    const u32x4 wu = __builtin_bit_cast(u32x4, w8);
 #pragma unroll
                     for (int q = 0; q < 4; ++q) P[q] = wu[q];
                 }
@@ -330,7 +333,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                 for (int m = 0; m < M; ++m) {
                     float v = FACT ? acc[m][t] : y[m][t];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) v = __builtin_amdgcn_fdot2(as_h2(P[q]), as_h2(xv[m][q]), v, false);
+                    for (int q = 0; q < 4; ++q) v = dot2<BF>(P[q], xv[m][q], v);
                     if constexpr (FACT) acc[m][t] = v; else y[m][t] = v;
                 }
             }
@@ -419,7 +422,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                 float v = 0.f;
 #pragma unroll
                 for (int w = 0; w < WAVES; ++w) v += sm.red[w][m][col];
-                C[(int64_t)m * N + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
+                C[(int64_t)m * N + n] = round_out<BF>(v);
             }
         }
         return;
@@ -453,7 +456,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         float v = 0.f;
         for (int s2 = 0; s2 < S; ++s2)
             v += __hip_atomic_load(&part[s2 * M * PW + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (n < N && m < mr) C[(int64_t)m * N + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
+        if (n < N && m < mr) C[(int64_t)m * N + n] = round_out<BF>(v);
     }
     if (tid == 0)   // leave the counter at zero for the next call
         __hip_atomic_store(&ws_cnt[p], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -508,7 +511,7 @@ inline GemvPlan plan_gemv(const Layout& L, int64_t M) {
 // counters where an earlier call (of any shape) left them at zero; then the
 // per-slice partial sums, which are always written before they are read.
 
-template <int BITS, int M, int SEG>
+template <int BITS, int M, int SEG, bool BF>
 int launch_g(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, void* ws,
              int mr, hipStream_t s) {
     constexpr int WAVES = gemv_waves_for(M);
@@ -520,32 +523,32 @@ int launch_g(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C,
     const int AS = split ? sp.AS : (int)L.na;
     int RW = (AS + WAVES - 1) / WAVES;               // atoms per wave
     if (SEG > 0) RW = (RW + SEG - 1) / SEG * SEG;    // runs start on group boundaries
-    return launch(gemv_kernel<BITS, M, WAVES, SEG, gemv_ring_for(M)>, dim3((unsigned)L.np, (unsigned)S),
+    return launch(gemv_kernel<BITS, M, WAVES, SEG, gemv_ring_for(M), BF>, dim3((unsigned)L.np, (unsigned)S),
                   dim3(WAVES * 64), 0, s, A, pk, C, (int)L.K, (int)L.N, L.group, L.s_off, L.z_off,
                   (int)L.na, (int)L.ng, S, AS, RW, part, cnt, mr);
 }
 
-template <int BITS, int M>
+template <int BITS, int M, bool BF>
 int launch_m(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, void* ws,
              hipStream_t s, int mr = M) {
     // group 128 (the AWQ default) gets its segments fixed at compile time
-    if (L.group == 128) return launch_g<BITS, M, 4>(L, A, pk, C, ws, mr, s);
-    return launch_g<BITS, M, 0>(L, A, pk, C, ws, mr, s);
+    if (L.group == 128) return launch_g<BITS, M, 4, BF>(L, A, pk, C, ws, mr, s);
+    return launch_g<BITS, M, 0, BF>(L, A, pk, C, ws, mr, s);
 }
 
-template <int BITS>
+template <int BITS, bool BF>
 int launch_bits(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, hipStream_t s) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
     switch (M) {
-        case 1: return launch_m<BITS, 1>(L, A, pk, C, ws, s);
-        case 2: return launch_m<BITS, 2>(L, A, pk, C, ws, s);
-        case 3: return launch_m<BITS, 3>(L, A, pk, C, ws, s);
-        case 4: return launch_m<BITS, 4>(L, A, pk, C, ws, s);
-        case 5: return launch_m<BITS, 5>(L, A, pk, C, ws, s);
-        case 6: return launch_m<BITS, 6>(L, A, pk, C, ws, s);
-        case 7: return launch_m<BITS, 7>(L, A, pk, C, ws, s);
-        case 8: return launch_m<BITS, 8>(L, A, pk, C, ws, s);
+        case 1: return launch_m<BITS, 1, BF>(L, A, pk, C, ws, s);
+        case 2: return launch_m<BITS, 2, BF>(L, A, pk, C, ws, s);
+        case 3: return launch_m<BITS, 3, BF>(L, A, pk, C, ws, s);
+        case 4: return launch_m<BITS, 4, BF>(L, A, pk, C, ws, s);
+        case 5: return launch_m<BITS, 5, BF>(L, A, pk, C, ws, s);
+        case 6: return launch_m<BITS, 6, BF>(L, A, pk, C, ws, s);
+        case 7: return launch_m<BITS, 7, BF>(L, A, pk, C, ws, s);
+        case 8: return launch_m<BITS, 8, BF>(L, A, pk, C, ws, s);
     }
     return TF_ERR_ARG;
 }
@@ -570,23 +573,35 @@ int64_t skinny_workspace_bytes(const Layout& L, int64_t M) {
 }
 
 int launch_gemv(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
-                void* ws, hipStream_t s) {
-    return L.bits == 4 ? launch_bits<4>(L, A, packed, C, M, ws, s)
-                       : launch_bits<8>(L, A, packed, C, M, ws, s);
+                void* ws, hipStream_t s, bool bf) {
+    if (bf)
+        return L.bits == 4 ? launch_bits<4, true>(L, A, packed, C, M, ws, s)
+                           : launch_bits<8, true>(L, A, packed, C, M, ws, s);
+    return L.bits == 4 ? launch_bits<4, false>(L, A, packed, C, M, ws, s)
+                       : launch_bits<8, false>(L, A, packed, C, M, ws, s);
 }
 
-int launch_skinny_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C,
+namespace {
+template <int BITS, bool BF>
+int launch_skinny_bits(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C,
                        int64_t M, void* ws, hipStream_t s) {
+    switch (skinny_slots(M)) {
+        case 16: return launch_m<BITS, 16, BF>(L, A, pk, C, ws, s, (int)M);
+        case 32: return launch_m<BITS, 32, BF>(L, A, pk, C, ws, s, (int)M);
+        default: return launch_m<BITS, 64, BF>(L, A, pk, C, ws, s, (int)M);
+    }
+}
+}  // namespace
+
+int launch_skinny_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C,
+                       int64_t M, void* ws, hipStream_t s, bool bf) {
     if (M < 1 || M > kSkinnyMaxM) return TF_ERR_ARG;
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    switch (skinny_slots(M)) {
-        case 16: return L.bits == 4 ? launch_m<4, 16>(L, A, pk, C, ws, s, (int)M)
-                                    : launch_m<8, 16>(L, A, pk, C, ws, s, (int)M);
-        case 32: return L.bits == 4 ? launch_m<4, 32>(L, A, pk, C, ws, s, (int)M)
-                                    : launch_m<8, 32>(L, A, pk, C, ws, s, (int)M);
-        default: return L.bits == 4 ? launch_m<4, 64>(L, A, pk, C, ws, s, (int)M)
-                                    : launch_m<8, 64>(L, A, pk, C, ws, s, (int)M);
-    }
+    if (bf)
+        return L.bits == 4 ? launch_skinny_bits<4, true>(L, A, pk, C, M, ws, s)
+                           : launch_skinny_bits<8, true>(L, A, pk, C, M, ws, s);
+    return L.bits == 4 ? launch_skinny_bits<4, false>(L, A, pk, C, M, ws, s)
+                       : launch_skinny_bits<8, false>(L, A, pk, C, M, ws, s);
 }
 
 }  // namespace tf

@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include <tuple>
+#include <type_traits>
 
 #include "tilefuse.h"
 
@@ -289,6 +290,188 @@ __device__ __forceinline__ half8_t dq_w8_dwords(uint32_t w0, uint32_t w1, uint32
     return __builtin_bit_cast(half8_t, st.out);
 }
 
+// ---------------------------------------------------------------------------
+// BF16 activations and scales (Sections 2.2 and 4.3: the paper's kernels take
+// BF16 activations, BF16 scales, and hold the dequantized weights in BF16).
+// Kernels are instantiated for fp16 (BF = false) and bfloat16 (BF = true);
+// both travel as 16-bit patterns, accumulation is fp32 either way.
+//
+// This GPU has no packed bfloat16 arithmetic, so the BF16 dequantization runs
+// in fp32: each code becomes an fp32 integer (v_cvt_f32_ubyte), one fused
+// multiply-add forms s * q - z * s = s * (q - z) exactly (s has 8 significant
+// bits and |q - z| < 2^8, so the product and z * s fit fp32's 24), and
+// v_cvt_pk_bf16_f32 rounds each pair to bfloat16, nearest even (Eq. 2,
+// rounded once).
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// bfloat16 bits -> fp32 (exact: the pattern is the high half of a binary32)
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+    return __builtin_bit_cast(float, bits16 << 16);
+}
+// The scale in fp32 from its 16-bit pattern.
+template <bool BF>
+__device__ __forceinline__ float scale_f32(uint32_t bits16) {
+    if constexpr (BF) return bf16_to_f32(bits16);
+    else return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
+}
+// fp32 -> output element, rounded to nearest even.
+template <bool BF>
+__device__ __forceinline__ uint16_t round_out(float v) {
+    if constexpr (BF) return __builtin_bit_cast(uint16_t, (__bf16)v);
+    else return __builtin_bit_cast(uint16_t, (_Float16)v);
+}
+// Two fp32 values -> one dword of two output elements (a in the low half).
+template <bool BF>
+__device__ __forceinline__ uint32_t round_out2(float a, float b) {
+    if constexpr (BF) {
+        const bf16x2_t v = {(__bf16)a, (__bf16)b};
+        return __builtin_bit_cast(uint32_t, v);
+    } else {
+        const half2_t v = {(_Float16)a, (_Float16)b};
+        return as_u32(v);
+    }
+}
+// c + a.lo * b.lo + a.hi * b.hi with fp32 accumulation (v_dot2 of two 16-bit pairs).
+template <bool BF>
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+    if constexpr (BF)
+        return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                               __builtin_bit_cast(bf16x2_t, b), c, false);
+    else return __builtin_amdgcn_fdot2(as_h2(a), as_h2(b), c, false);
+}
+// acc += a x b on the matrix core, 16 x 16 x 32, 16-bit inputs.
+template <bool BF>
+__device__ __forceinline__ float4_t mfma16(const u32x4& a, const u32x4& b, const float4_t& c) {
+    if constexpr (BF)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                       __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, a),
+                                                      __builtin_bit_cast(half8_t, b), c, 0, 0, 0);
+}
+
+// bfloat16 pattern 0x4300 | v is exactly 128 + v for 0 <= v < 128: a nibble
+// in bits 0..3 of each half of x reads as (128 + q, 128 + q').
+constexpr uint32_t kMagicBf2 = 0x43004300u;
+__device__ __forceinline__ uint32_t magic_bf_reg() {
+    uint32_t m;
+    asm("v_mov_b32 %0, 0x43004300" : "=v"(m));
+    return m;
+}
+
+// Per-column dequantization constants of one group.
+//  fp16: (s, s), -(1024 + z) and -(64 + z) as fp16 pairs (see dq_w4_step);
+//  bf16: s and -(z * s) in fp32 (exact).
+template <bool BF>
+struct DqConst;
+template <>
+struct DqConst<false> {
+    half2_t s2;
+    uint32_t nz, nz64;
+};
+template <>
+struct DqConst<true> {
+    float s, nzs;
+};
+template <bool BF>
+__device__ __forceinline__ DqConst<BF> make_dq_const(uint32_t sbits16, uint32_t z) {
+    DqConst<BF> k;
+    if constexpr (BF) {
+        k.s = bf16_to_f32(sbits16);
+        k.nzs = -((float)z * k.s);
+    } else {
+        k.s2 = as_h2(sbits16 | (sbits16 << 16));
+        k.nz = neg_zero_pair(z);
+        k.nz64 = neg_zero64_pair(k.nz);
+    }
+    return k;
+}
+
+// BF16 dequantization micro-steps (one vector instruction each, like
+// dq_w4_step / dq_w8_step).  Packed nibble j holds row 2j (j < 4) or
+// 2(j - 4) + 1, so after lo = w & 0x0F0F0F0F and hi = (w >> 4) & 0x0F0F0F0F
+// the bytes hold rows lo: 0, 4, 1, 5 and hi: 2, 6, 3, 7.
+// 4-bit, 23 steps: 0..2 split into lo, hi; then per output pair j (rows
+// 2j, 2j + 1), five steps: two byte -> fp32 conversions, two exact fmas,
+// one rounding conversion of the pair.
+// 8-bit, 20 steps on w0 (rows 0..3) and w1 (rows 4..7): five per pair.
+struct DqStateBf {
+    uint32_t lo, hi;
+    float f0, f1;
+    u32x4 out;
+};
+constexpr int kDqW4StepsBf = 23, kDqW8StepsBf = 20;
+
+__device__ __forceinline__ float byte_f32(uint32_t v, int b) {
+    return (float)((v >> (8 * b)) & 0xFFu);      // v_cvt_f32_ubyte{b}
+}
+
+// pair j's source word and bytes (4-bit: after the split)
+__device__ __forceinline__ void dq_bf_pair_step(int k, uint32_t src, int b0, int b1, int j,
+                                                const DqConst<true>& kc, DqStateBf& st) {
+    switch (k) {
+        case 0: st.f0 = byte_f32(src, b0); break;
+        case 1: st.f1 = byte_f32(src, b1); break;
+        case 2: st.f0 = __builtin_fmaf(st.f0, kc.s, kc.nzs); break;
+        case 3: st.f1 = __builtin_fmaf(st.f1, kc.s, kc.nzs); break;
+        default: {
+            const bf16x2_t v = {(__bf16)st.f0, (__bf16)st.f1};
+            st.out[j] = __builtin_bit_cast(uint32_t, v);
+        }
+    }
+}
+
+__device__ __forceinline__ void dq_w4_step_bf(int k, uint32_t w, const DqConst<true>& kc,
+                                              DqStateBf& st) {
+    if (k == 0) { st.lo = w & 0x0F0F0F0Fu; return; }
+    if (k == 1) { st.hi = w >> 4; return; }
+    if (k == 2) { st.hi &= 0x0F0F0F0Fu; return; }
+    const int j = (k - 3) / 5, r = (k - 3) % 5;
+    // pairs: (lo.b0, lo.b2), (hi.b0, hi.b2), (lo.b1, lo.b3), (hi.b1, hi.b3)
+    dq_bf_pair_step(r, (j & 1) ? st.hi : st.lo, j >> 1, (j >> 1) + 2, j, kc, st);
+}
+
+__device__ __forceinline__ void dq_w8_step_bf(int k, uint32_t w0, uint32_t w1,
+                                              const DqConst<true>& kc, DqStateBf& st) {
+    const int j = k / 5, r = k % 5;
+    dq_bf_pair_step(r, j < 2 ? w0 : w1, 2 * (j & 1), 2 * (j & 1) + 1, j, kc, st);
+}
+
+// Generic interface over both element types: the state, the number of
+// micro-steps, one step, and the whole operand (eight weights of one column,
+// 16-bit elements, rows 0..7 in order, two per dword).  w1 is the second
+// dword of an 8-bit operand (unused for 4-bit).  `magic` = magic_reg() (fp16).
+template <bool BF>
+using DqSt = typename std::conditional<BF, DqStateBf, DqState>::type;
+
+template <bool BF, int BITS>
+constexpr int dq_steps() {
+    return BF ? (BITS == 4 ? kDqW4StepsBf : kDqW8StepsBf) : (BITS == 4 ? kDqW4Steps : kDqW8Steps);
+}
+
+template <bool BF, int BITS>
+__device__ __forceinline__ void dq_step(int k, uint32_t w0, uint32_t w1, uint32_t magic,
+                                        const DqConst<BF>& kc, DqSt<BF>& st) {
+    if constexpr (BF) {
+        if constexpr (BITS == 4) dq_w4_step_bf(k, w0, kc, st);
+        else dq_w8_step_bf(k, w0, w1, kc, st);
+    } else {
+        if constexpr (BITS == 4) dq_w4_step(k, w0, magic, kc.nz, kc.nz64, kc.s2, st);
+        else dq_w8_step(k, w0, w1, kc.nz, kc.s2, st);
+    }
+}
+
+template <bool BF, int BITS>
+__device__ __forceinline__ u32x4 dq_operand(uint32_t w0, uint32_t w1, uint32_t magic,
+                                            const DqConst<BF>& kc) {
+    DqSt<BF> st;
+#pragma unroll
+    for (int k = 0; k < dq_steps<BF, BITS>(); ++k) dq_step<BF, BITS>(k, w0, w1, magic, kc, st);
+    return st.out;
+}
+
 }  // namespace tf
 
 // Launchers implemented in the kernel sources (called by tf_api.hip after
@@ -307,16 +490,16 @@ int launch_dequant(const Layout& L, const void* packed, int out_dtype, void* w_o
 int64_t gemv_workspace_bytes(const Layout& L, int64_t M);
 int64_t skinny_workspace_bytes(const Layout& L, int64_t M);
 int launch_gemv(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
-                void* ws, hipStream_t s);
+                void* ws, hipStream_t s, bool bf);
 int launch_skinny_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C,
-                       int64_t M, void* ws, hipStream_t s);
+                       int64_t M, void* ws, hipStream_t s, bool bf);
 int64_t gemm_workspace_bytes(const Layout& L, int64_t M);
 bool gemm256_supported(const Layout& L);
 bool gemm256_fills_device(const Layout& L, int64_t M);
 int64_t gemm256_workspace_bytes(const Layout& L, int64_t M);
 int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
-                   void* ws, size_t ws_bytes, hipStream_t s);
+                   void* ws, size_t ws_bytes, hipStream_t s, bool bf);
 int launch_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
-                void* ws, size_t ws_bytes, hipStream_t s);
+                void* ws, size_t ws_bytes, hipStream_t s, bool bf);
 int launch_silu_mul(const uint16_t* gu, int64_t M, int64_t N, uint16_t* h, hipStream_t s);
 }  // namespace tf

@@ -148,10 +148,11 @@ __global__ void unpack_zeros(const uint8_t* __restrict__ zreg, uint8_t* __restri
 }
 
 // tf_dequant: one thread per 8 codes of one column (one MFMA B operand),
-// dequantized with dq_w4_dword / dq_w8_dwords exactly as in the GEMM.
+// dequantized with the matmul kernels' own code.  mode 0: fp16 scales, fp16
+// weights; 1: fp16 scales, exact fp32 weights; 2: bf16 scales, bf16 weights.
 __global__ void dequant_weights(int bits, const uint8_t* __restrict__ packed, int64_t s_off,
                                 int64_t z_off, int64_t N, int64_t na, int64_t ng, int group,
-                                int out_f32, void* __restrict__ w_out, int64_t slices) {
+                                int mode, void* __restrict__ w_out, int64_t slices) {
     int64_t sidx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (sidx >= slices) return;
     // slice = (atom, lane, column-slot); 64 lanes x 4 (4-bit) or 2 (8-bit) slots
@@ -170,6 +171,14 @@ __global__ void dequant_weights(int bits, const uint8_t* __restrict__ packed, in
     uint16_t sbits = reinterpret_cast<const uint16_t*>(packed + s_off)[meta];
     uint32_t z = packed[z_off + meta];
     const uint32_t* atomw = reinterpret_cast<const uint32_t*>(packed) + atom * 256 + lane * 4;
+    if (mode == 2) {
+        const DqConst<true> kq = make_dq_const<true>(sbits, z);
+        const u32x4 wb = bits == 4 ? dq_operand<true, 4>(atomw[t], 0u, 0u, kq)
+                                   : dq_operand<true, 8>(atomw[2 * t], atomw[2 * t + 1], 0u, kq);
+        uint16_t* o = reinterpret_cast<uint16_t*>(w_out);
+        for (int j = 0; j < 8; ++j) o[(k0 + j) * N + n] = (uint16_t)(wb[j >> 1] >> (16 * (j & 1)));
+        return;
+    }
     half8_t w8;
     uint32_t codes[4];
     if (bits == 4) {
@@ -184,7 +193,7 @@ __global__ void dequant_weights(int bits, const uint8_t* __restrict__ packed, in
         w8_code_pairs(w0, codes);
         w8_code_pairs(w1, codes + 2);
     }
-    if (out_f32) {
+    if (mode == 1) {
         // exact: (q - z) is formed exactly in fp16 by the same pair subtraction
         // and its product with the fp16 scale needs at most 19 significant bits
         float s = (float)__builtin_bit_cast(_Float16, sbits);
@@ -264,7 +273,7 @@ int launch_dequant(const Layout& L, const void* packed, int out_dtype, void* w_o
     int64_t slices = L.np * L.na * 64 * L.T;
     return launch(dequant_weights, dim3(blocks_for(slices, 256)), dim3(256), 0, s, L.bits,
                   static_cast<const uint8_t*>(packed), L.s_off, L.z_off, L.N, L.na, L.ng,
-                  L.group, out_dtype == TF_F32 ? 1 : 0, w_out, slices);
+                  L.group, out_dtype == TF_F32 ? 1 : out_dtype == TF_BF16 ? 2 : 0, w_out, slices);
 }
 
 }  // namespace tf

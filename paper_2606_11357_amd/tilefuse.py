@@ -22,12 +22,14 @@ TF_ERR_ARG = -5
 TF_ERR_HIP = -6
 TF_F16 = 1
 TF_F32 = 2
+TF_BF16 = 3
 GEMV_MAX_M = 8
 
 EXPORTS = (
     "tf_layout_version", "tf_status_str", "tf_packed_bytes", "tf_pack_w4", "tf_pack_w8",
     "tf_pack_w8_sym", "tf_workspace_bytes", "tf_w4a16_gemm", "tf_w8a16_gemm", "tf_w4a16_gemv",
-    "tf_w8a16_gemv", "tf_unpack", "tf_dequant", "tf_silu_mul",
+    "tf_w8a16_gemv", "tf_w4a16_gemm_bf16", "tf_w8a16_gemm_bf16", "tf_w4a16_gemv_bf16",
+    "tf_w8a16_gemv_bf16", "tf_unpack", "tf_dequant", "tf_silu_mul",
 )
 
 
@@ -62,6 +64,10 @@ def load() -> ctypes.CDLL:
         "tf_w8a16_gemm": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_w4a16_gemv": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_w8a16_gemv": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
+        "tf_w4a16_gemm_bf16": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
+        "tf_w8a16_gemm_bf16": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
+        "tf_w4a16_gemv_bf16": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
+        "tf_w8a16_gemv_bf16": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_unpack": (I, [I, P, I64, I64, I, P, P, P]),
         "tf_dequant": (I, [I, P, I64, I64, I, I, P, P]),
         "tf_silu_mul": (I, [P, I64, I64, P, P]),
@@ -143,7 +149,8 @@ def default_workspace(device, nbytes: int):
 
 
 def pack_w4(qweight, qzeros, scales, K: int, N: int, group: int = 128, out=None):
-    """Pre-tile an AWQ 4-bit weight (int32 [K, N/8], int32 [K/G, N/8], fp16 [K/G, N])."""
+    """Pre-tile an AWQ 4-bit weight (int32 [K, N/8], int32 [K/G, N/8], fp16 or bf16
+    [K/G, N]; the scale bits are copied as they are)."""
     torch = _torch()
     _need_cuda(qweight, qzeros, scales)
     if out is None:
@@ -154,7 +161,7 @@ def pack_w4(qweight, qzeros, scales, K: int, N: int, group: int = 128, out=None)
 
 
 def pack_w8(qweight, zeros, scales, K: int, N: int, group: int = 128, out=None):
-    """Pre-tile an 8-bit weight (uint8 [K, N], uint8 [K/G, N], fp16 [K/G, N])."""
+    """Pre-tile an 8-bit weight (uint8 [K, N], uint8 [K/G, N], fp16 or bf16 [K/G, N])."""
     torch = _torch()
     _need_cuda(qweight, zeros, scales)
     if out is None:
@@ -166,7 +173,7 @@ def pack_w8(qweight, zeros, scales, K: int, N: int, group: int = 128, out=None):
 
 def pack_w8_sym(qweight, scales, K: int, N: int, group: int = 128, out=None):
     """Pre-tile a signed INT8 weight with one scale per output channel
-    (int8 [K, N], fp16 [N]); use it with the 8-bit matmul calls and `group`."""
+    (int8 [K, N], fp16 or bf16 [N]); use it with the 8-bit matmul calls and `group`."""
     torch = _torch()
     _need_cuda(qweight, scales)
     if out is None:
@@ -177,15 +184,19 @@ def pack_w8_sym(qweight, scales, K: int, N: int, group: int = 128, out=None):
 
 
 def _matmul(bits, kind, A, packed, K, N, group, out, workspace):
-    """workspace: None -> the cached per-device default, False -> none (single-pass
+    """A fp16 or bfloat16 [M, K] selects the entry point (the packed scales must
+    hold the same dtype's bits); the output has A's dtype.
+    workspace: None -> the cached per-device default, False -> none (single-pass
     kernels), or a caller tensor (zero-filled before its first use)."""
     torch = _torch()
     _need_cuda(A, packed, out)
     M = A.shape[0]
-    if A.dtype != torch.float16 or A.dim() != 2 or A.shape[1] != K:
-        raise ValueError("A must be fp16 [M, K]")
+    if A.dtype not in (torch.float16, torch.bfloat16) or A.dim() != 2 or A.shape[1] != K:
+        raise ValueError("A must be fp16 or bf16 [M, K]")
     if out is None:
-        out = torch.empty((M, N), dtype=torch.float16, device=A.device)
+        out = torch.empty((M, N), dtype=A.dtype, device=A.device)
+    elif out.dtype != A.dtype or tuple(out.shape) != (M, N):
+        raise ValueError("out must have A's dtype and shape [M, N]")
     if workspace is None:
         need = workspace_bytes(bits, M, K, N, group)
         workspace = default_workspace(A.device, need) if need else False
@@ -194,7 +205,7 @@ def _matmul(bits, kind, A, packed, K, N, group, out, workspace):
     else:
         _need_cuda(workspace)
         ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
-    name = f"tf_w{bits}a16_{kind}"
+    name = f"tf_w{bits}a16_{kind}" + ("_bf16" if A.dtype == torch.bfloat16 else "")
     rc = getattr(load(), name)(_ptr(A), _ptr(packed), _ptr(out), M, K, N, group, ws_ptr, ws_bytes,
                                _stream(A.device))
     _check(rc, name)
@@ -229,11 +240,12 @@ def unpack(bits: int, packed, K: int, N: int, group: int = 128):
 
 
 def dequant(bits: int, packed, K: int, N: int, group: int = 128, dtype=None):
-    """Dequantized weights [K, N] (fp16 rounded once, or exact fp32)."""
+    """Dequantized weights [K, N]: fp16 rounded once or exact fp32 (fp16 scales),
+    or bfloat16 rounded once (bfloat16 scales)."""
     torch = _torch()
     dtype = dtype or torch.float16
     _need_cuda(packed)
-    code = {torch.float16: TF_F16, torch.float32: TF_F32}[dtype]
+    code = {torch.float16: TF_F16, torch.float32: TF_F32, torch.bfloat16: TF_BF16}[dtype]
     w = torch.empty((K, N), dtype=dtype, device=packed.device)
     _check(load().tf_dequant(bits, _ptr(packed), K, N, group, code, _ptr(w),
                              _stream(packed.device)), "tf_dequant")

@@ -95,15 +95,15 @@ def test_packed_bytes_rejects(lib, args, want):
 MATMUL_OK = dict(A=P, packed=P, C=P, M=4, K=256, N=64, G=128)
 
 
-def _gemv(lib, bits, **kw):
+def _gemv(lib, bits, dt="", **kw):
     a = {**MATMUL_OK, **kw}
-    fn = lib.tf_w4a16_gemv if bits == 4 else lib.tf_w8a16_gemv
+    fn = getattr(lib, f"tf_w{bits}a16_gemv{dt}")
     return fn(a["A"], a["packed"], a["C"], a["M"], a["K"], a["N"], a["G"], NULL, 0, NULL)
 
 
-def _gemm(lib, bits, ws=NULL, ws_bytes=0, **kw):
+def _gemm(lib, bits, ws=NULL, ws_bytes=0, dt="", **kw):
     a = {**MATMUL_OK, **kw}
-    fn = lib.tf_w4a16_gemm if bits == 4 else lib.tf_w8a16_gemm
+    fn = getattr(lib, f"tf_w{bits}a16_gemm{dt}")
     return fn(a["A"], a["packed"], a["C"], a["M"], a["K"], a["N"], a["G"], ws, ws_bytes, NULL)
 
 
@@ -124,17 +124,19 @@ BAD_MATMUL = [
 ]
 
 
+@pytest.mark.parametrize("dt", ["", "_bf16"])
 @pytest.mark.parametrize("bits", [4, 8])
 @pytest.mark.parametrize("kw,want", BAD_MATMUL, ids=[str(b[0]) for b in BAD_MATMUL])
-def test_matmul_rejects(lib, bits, kw, want):
-    assert _gemv(lib, bits, **kw) == want
-    assert _gemm(lib, bits, **kw) == want
+def test_matmul_rejects(lib, bits, kw, want, dt):
+    assert _gemv(lib, bits, dt=dt, **kw) == want
+    assert _gemm(lib, bits, dt=dt, **kw) == want
 
 
+@pytest.mark.parametrize("dt", ["", "_bf16"])
 @pytest.mark.parametrize("bits", [4, 8])
-def test_gemv_rejects_large_m(lib, bits):
-    assert _gemv(lib, bits, M=9) == tfb.TF_ERR_ARG
-    assert _gemv(lib, bits, M=4096) == tfb.TF_ERR_ARG
+def test_gemv_rejects_large_m(lib, bits, dt):
+    assert _gemv(lib, bits, dt=dt, M=9) == tfb.TF_ERR_ARG
+    assert _gemv(lib, bits, dt=dt, M=4096) == tfb.TF_ERR_ARG
 
 
 def test_workspace_query(lib):
@@ -197,6 +199,8 @@ def test_unpack_dequant_reject(lib):
     assert lib.tf_dequant(8, P, 256, 64, 128, tfb.TF_F16, NULL, NULL) == tfb.TF_ERR_NULL
     assert lib.tf_dequant(8, P, 256, 64, 128, tfb.TF_F32, P_ODD, NULL) == tfb.TF_ERR_ALIGN
     assert lib.tf_dequant(4, P, 250, 64, 128, tfb.TF_F32, P, NULL) == tfb.TF_ERR_SHAPE
+    assert lib.tf_dequant(4, P, 256, 64, 128, tfb.TF_BF16, P_ODD, NULL) == tfb.TF_ERR_ALIGN
+    assert lib.tf_dequant(4, P, 256, 64, 128, 4, P, NULL) == tfb.TF_ERR_ARG
 
 
 def test_binding_refuses_cpu_tensors():
