@@ -38,7 +38,7 @@ GEMV_SHAPE = (1, 4096, 14336)
 GROUP = 128
 GEMV_REPS = 32
 GEMM_COPIES = 8
-PEAK_F16_TFLOPS = 2516.6      # 256 CU x 4096 FLOP/clk x 2.4 GHz (dense fp16 MFMA)
+PEAK_F16_TFLOPS = 2516.6      # 256 CU x 4096 FLOP/clk x 2.4 GHz (dense fp16 or bf16 MFMA)
 PEAK_HBM_GBS = 8000.0
 COPY_BYTES = 1 << 30
 
@@ -142,36 +142,42 @@ def algo_bytes(bits, K, N, G=GROUP):
     return K * N + (K // G) * N * 2 + (K // G) * N
 
 
-def sweep(torch, tf, make_inputs, reps=50):
-    """Every workload of synth.WORKLOADS: HIP-event time per launch over
-    3 replays of a graph of `reps` launches rotating over enough distinct
-    copies of the packed weight that the copies exceed 512 MB (so weights
-    stream from HBM, not the MALL), the library's default workspace, inputs
-    resident."""
-    from paper_2606_11357_amd.synth import WORKLOADS
+def sweep(torch, tf, make_inputs, reps=50, dtypes=("f16", "bf16")):
+    """Every workload of synth.WORKLOADS, with fp16 and with BF16 activations
+    and scales: HIP-event time per launch over 3 replays of a graph of `reps`
+    launches rotating over enough distinct copies of the packed weight that
+    the copies exceed 512 MB (so weights stream from HBM, not the MALL), the
+    library's default workspace, inputs resident."""
+    from paper_2606_11357_amd.synth import WORKLOADS, make_inputs_bf16
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
     up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-    for name, (bits, Ms, K, N, xstd) in WORKLOADS.items():
-        for M in Ms:
-            d = make_inputs(bits, M, K, N, group=GROUP, seed=0, x_std=xstd)
-            if bits == 4:
-                p0 = tf.pack_w4(up(d["qweight"]), up(d["qzeros"]), up(d["s"]), K, N, GROUP)
-            else:
-                p0 = tf.pack_w8(up(d["qweight"]), up(d["zeros"]), up(d["s"]), K, N, GROUP)
-            ncopy = int(min(40, max(2, -(-(512 << 20) // p0.numel()))))
-            copies = [p0] + [p0.clone() for _ in range(ncopy - 1)]
-            x = up(d["x"])
-            y = torch.empty((M, N), dtype=torch.float16, device=dev)
-            # decode shapes go through both entry points (the GEMV is vector-ALU
-            # only; the GEMM entry may use the matrix cores from 4 rows up)
-            for entry in (("gemv", "gemm") if M <= tf.GEMV_MAX_M else ("gemm",)):
-                sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps)
-            del copies, p0, x, y, d
-            torch.cuda.empty_cache()
+    for dt in dtypes:
+        for name, (bits, Ms, K, N, xstd) in WORKLOADS.items():
+            for M in Ms:
+                if dt == "bf16":
+                    d = make_inputs_bf16(bits, M, K, N, group=GROUP, seed=0, x_std=xstd)
+                    s = up(d["s_bits"].view(np.int16))
+                    x = up(d["x_bits"].view(np.int16)).view(torch.bfloat16)
+                else:
+                    d = make_inputs(bits, M, K, N, group=GROUP, seed=0, x_std=xstd)
+                    s, x = up(d["s"]), up(d["x"])
+                if bits == 4:
+                    p0 = tf.pack_w4(up(d["qweight"]), up(d["qzeros"]), s, K, N, GROUP)
+                else:
+                    p0 = tf.pack_w8(up(d["qweight"]), up(d["zeros"]), s, K, N, GROUP)
+                ncopy = int(min(40, max(2, -(-(512 << 20) // p0.numel()))))
+                copies = [p0] + [p0.clone() for _ in range(ncopy - 1)]
+                y = torch.empty((M, N), dtype=x.dtype, device=dev)
+                # decode shapes go through both entry points (the GEMV is vector-ALU
+                # only; the GEMM entry may use the matrix cores from 4 rows up)
+                for entry in (("gemv", "gemm") if M <= tf.GEMV_MAX_M else ("gemm",)):
+                    sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps, dt)
+                del copies, p0, x, y, d, s
+                torch.cuda.empty_cache()
 
 
-def sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps):
+def sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps, dtype="f16"):
     fn = getattr(tf, f"w{bits}a16_{entry}")
     ncopy = len(copies)
     for i in range(5):
@@ -196,7 +202,8 @@ def sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps)
     gbs = algo_bytes(bits, K, N) / us / 1e3
     hbm_bound = M <= 16
     print(json.dumps({
-        "workload": name, "entry": entry, "bits": bits, "M": M, "K": K, "N": N, "group": GROUP,
+        "workload": name, "dtype": dtype, "entry": entry, "bits": bits, "M": M, "K": K, "N": N,
+        "group": GROUP,
         "us_per_launch": round(us, 3), "TFLOP/s": round(tflops, 2), "GB/s": round(gbs, 1),
         "bound": "hbm" if hbm_bound else "mfma",
         "frac": round(gbs / PEAK_HBM_GBS if hbm_bound else tflops / PEAK_F16_TFLOPS, 4),
