@@ -39,11 +39,9 @@ constexpr int kGemmThreads = 256;
 constexpr int kXcds = 8;
 constexpr int kABufs = 3;
 
-// LDS slot (16-byte chunks) of chunk `ch` (0..3) of A row `row`: rows are 64
-// bytes; the XOR with row bits 2..3 sends the 16 lanes of one ds_read_b128
-// (16 consecutive rows, same chunk) to 16 distinct 4-bank groups of the
-// 64-bank LDS.
-__device__ __forceinline__ int a_slot(int row, int ch) { return row * 4 + (ch ^ ((row >> 2) & 3)); }
+// LDS slot (16-byte chunks) of chunk `ch` (0..3) of A row `row` (64-byte
+// rows; see lds_a_slot).
+__device__ __forceinline__ int a_slot(int row, int ch) { return lds_a_slot(row, ch); }
 
 // MPC: metadata groups per chunk (1 when a group spans the whole chunk, else
 // chunk rows / group); the group of step j is j / (chunk steps / MPC).
@@ -331,7 +329,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
 // 32-row steps, single-buffered.
 constexpr int kBM1 = 128, kBN1 = 128, kBK1 = 32;
 
-__device__ __forceinline__ int a_swz1(int row, int chunk) { return row * 4 + (chunk ^ ((row >> 2) & 3)); }
+__device__ __forceinline__ int a_swz1(int row, int chunk) { return lds_a_slot(row, chunk); }
 
 template <int BITS, bool BF>
 __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_generic(

@@ -34,10 +34,9 @@ constexpr int kCS = 4;                 // steps per 128-row chunk (atom ring siz
 constexpr int kRB = kBM / 16;          // 16-row blocks per wave
 constexpr int kSkMinUnits = 8;         // fewest K chunks per stream-K block
 
-// 16-byte LDS slot of chunk `ch` (0..3) of A row `row` (64-byte rows); the
-// XOR with row bits 2..3 spreads the 16 rows of one ds_read_b128 quarter-wave
-// over distinct bank groups.
-__device__ __forceinline__ int a_slot(int row, int ch) { return row * 4 + (ch ^ ((row >> 2) & 3)); }
+// 16-byte LDS slot of chunk `ch` (0..3) of A row `row` (64-byte rows; see
+// lds_a_slot).
+__device__ __forceinline__ int a_slot(int row, int ch) { return lds_a_slot(row, ch); }
 
 __device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
@@ -71,16 +70,22 @@ __device__ __forceinline__ void mfma_hazard_gap() {
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7");
 }
 
-// End-of-step barrier.  The A tile of a step reaches LDS by direct
-// global-to-LDS loads (four per thread, the last vector-memory operations of
-// every step); waiting until at most four are outstanding means that all but
-// this step's four -- among them those of the previous step, whose tile is
-// read from the next step on -- have landed.  LDS reads issued before the
-// barrier stay in flight (no LDS wait).  s_waitcnt fields: vmcnt = 4, expcnt
-// and lgkmcnt at their maximum (no wait).
+// End-of-step barrier.  The A tile of step s + 3 reaches LDS by direct
+// global-to-LDS loads issued during step s; its first fragments are read
+// during step s + 2, so at the end of every step the direct loads issued in
+// the step before must have landed (each wave waits for its own, then the
+// barrier makes all of them visible).  Vector-memory operations complete in
+// order, so the wait leaves in flight exactly the NOW operations this step
+// issued (its atom loads, its four direct loads and, on a chunk's last step,
+// the metadata loads of the chunk after next), which are needed a step or
+// more later: a weight atom three steps on, metadata four.  LDS reads
+// issued before the barrier stay in flight (no LDS wait).  s_waitcnt fields:
+// vmcnt = NOW (bits 3..0 and 15..14), expcnt and lgkmcnt at their maximum.
+template <int NOW>
 __device__ __forceinline__ void barrier_after_a_loads() {
+    static_assert(NOW >= 4 && NOW < 64, "vmcnt holds 6 bits");
     __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(0x0F74);
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (NOW & 15) | ((NOW >> 4) << 14));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
 }
@@ -154,12 +159,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     // direct loads per thread; load r of wave w fills slots (4 w + r) * 64 +
     // lane (a direct load writes lane l's 16 bytes at its base + 16 l), so
     // each lane fetches the A chunk that belongs in its slot: slot X holds
-    // row X / 4, chunk (X % 4) ^ ((row / 4) % 4) (the inverse of a_slot).
+    // row X / 4, chunk (X % 4) ^ lds_chunk_swz(row) (the inverse of a_slot).
     uint32_t avoff[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int x = (4 * wave + r) * 64 + lane;
-        const int row = x >> 2, chk = (x & 3) ^ ((row >> 2) & 3);
+        const int row = x >> 2, chk = (x & 3) ^ lds_chunk_swz(row);
         avoff[r] = (uint32_t)row * (uint32_t)K * 2u + (uint32_t)chk * 16u;
     }
     auto read_a = [&](int buf, int i) { return abuf(buf)[a_slot(16 * i + c, kg)]; };
@@ -396,7 +401,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int t = 0; t < 4; ++t) bop[t] = bnext[t];
-                barrier_after_a_loads();
+                // vector-memory operations of this step: metadata (last step
+                // of a chunk: two loads per group and panel), one atom load
+                // per panel, four direct loads
+                constexpr int kMetaLoads = 2 * MPC * PANELS;
+                if (j == kCS - 1) barrier_after_a_loads<kMetaLoads + PANELS + 4>();
+                else barrier_after_a_loads<PANELS + 4>();
             }
         }
         mfma_hazard_gap();

@@ -290,6 +290,19 @@ __device__ __forceinline__ half8_t dq_w8_dwords(uint32_t w0, uint32_t w1, uint32
     return __builtin_bit_cast(half8_t, st.out);
 }
 
+// 16-byte LDS slot of chunk `ch` (0..3) of activation row `row` in a tile of
+// 64-byte rows (32 fp16 / bf16 values of K per row).  The matrix-core kernels
+// read one chunk of 16 consecutive rows per quarter of a wavefront
+// (ds_read_b128: lane c of the quarter reads row r0 + c).  XOR-ing the chunk
+// with ((row >> 1) ^ (row >> 3)) & 3 puts every 8 consecutive rows of one
+// chunk in 8 distinct 16-byte slots modulo 8, and every 16 in 16 distinct
+// slots modulo 16, so no two lanes served together share an LDS bank (ds_read_b128
+// measured on MI355X at the rate of a contiguous read; the XOR with row bits
+// 2..3 alone, distinct only modulo 16, ran 36% slower).  The XOR is its own
+// inverse: chunk ^ f(row) also maps a slot back to its chunk.
+__device__ __forceinline__ int lds_chunk_swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
+__device__ __forceinline__ int lds_a_slot(int row, int ch) { return row * 4 + (ch ^ lds_chunk_swz(row)); }
+
 // ---------------------------------------------------------------------------
 // BF16 activations and scales (Sections 2.2 and 4.3: the paper's kernels take
 // BF16 activations, BF16 scales, and hold the dequantized weights in BF16).
