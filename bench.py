@@ -499,7 +499,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(tflops / PEAK_F16_TFLOPS, 4),
             "traffic": recorded_traffic("tf_gemm256.hip"),
-            "kernel": "gemm256_kernel<4,1> (K=4096 N=14336: whole 256x256 tiles; "
+            "kernel": "gemm256_kernel<4,1,false> (K=4096 N=14336: whole 256x256 tiles; "
                       "K=14336 N=4096: stream-K over 256 blocks)",
         },
         "gemv": {
@@ -510,7 +510,7 @@ def main():
             "roofline": {"bound": "hbm", "achieved": round(gemv_gbs, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(gemv_gbs / PEAK_HBM_GBS, 4),
                          "traffic": recorded_traffic("tf_gemv.hip"),
-                         "kernel": "gemv_kernel<4,1,16,4,2>"},
+                         "kernel": "gemv_kernel<4,1,16,4,2,false>"},
         },
         "gemm_ms_per_step": round(gemm_ms, 4),
         "gemm_us_per_shape": {f"K={K},N={N}": round(t * 1e3, 2) for (M, K, N), t in zip(GEMM_SHAPES, shape_ms)},
