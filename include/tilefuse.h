@@ -137,9 +137,12 @@ int64_t tf_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group)
  * Prefill GEMM (Section 2.1: M grows with the prompt length):
  *   C_f16[M, N] = A_f16[M, K] x dequant(packed)[K, N], fp32 accumulate, RNE.
  * Any M >= 1.  M <= 3 runs the decode GEMV; 4 <= M <= 64 a weight-streaming
- * kernel that feeds each dequantized dword to matrix-core instructions (16,
- * 32 or 64 row slots); larger M the tiled matrix-core GEMMs.  The dequantized
- * fp16 weight fed to the matrix cores is RNE(s * (q - z)), rounded once.
+ * kernel on the matrix cores (16, 32 or 64 row slots); larger M the tiled
+ * matrix-core GEMMs.  The tiled GEMMs and the 64-slot form feed the matrix
+ * cores the dequantized fp16 weight RNE(s * (q - z)), rounded once; up to
+ * 32 rows the streaming kernel feeds the codes themselves and applies scale
+ * and zero-point to each group's sums (Eq. 2 summed over a group), so no
+ * weight is rounded (as in the decode GEMV up to 4 rows).
  * workspace: see tf_workspace_bytes.
  */
 int tf_w4a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,

@@ -2,10 +2,16 @@
 // matrix-vector products; Section 4.3 "GEMV microkernel"; Section 4.4).
 //
 // y[m, n] = sum_k x[m, k] * s[g, n] * (q[k, n] - z[g, n]),  1 <= M <= 8, on
-// the vector ALU only.  The same streaming kernel with 16 row slots serves
-// the GEMM entry points for few rows (skinny prefill, 4 <= M <= 16): there
-// each dequantized dword is the B operand of one v_mfma_f32_16x16x32_f16 and
-// the weights, not the matrix cores, bound the time.
+// the vector ALU only.  The same streaming kernel with 16, 32 or 64 row
+// slots serves the GEMM entry points for few rows (skinny prefill,
+// 4 <= M <= 64) on the matrix cores (v_mfma_f32_16x16x32_f16 / _bf16), where
+// the weights, not the matrix cores, bound the time.  With 16 or 32 slots the
+// codes themselves (exact 16-bit integers o + q) are the B operand: per group
+// the matrix core forms sum A * (o + q) and, against an operand of ones, the
+// row sums of A, and the group closes with s * (acc - (o + z) * rowsum), which
+// leaves the vector ALU a few instructions per dword instead of the whole
+// dequantization.  With 64 slots (too many group sums for the registers) each
+// weight is dequantized with the GEMM's code and fed to the matrix core.
 //
 // Mapping (the GPU form of the principle of Section 4.4: every compute unit
 // streams its own weight slice, the activations are shared, each workgroup
@@ -58,6 +64,11 @@ struct GemvCfg {
     // read per atom, MB blocks of 16 rows
     static constexpr bool MF = M > TF_GEMV_MAX_M;
     static constexpr int MB = MF ? M / 16 : 1;
+    // matrix-core factored form (16 or 32 row slots): the codes themselves
+    // are the B operand and the scale and zero-point are applied per group
+    // (64 slots keep the dequantized operand: the group sums would not fit
+    // in registers)
+    static constexpr bool MFF = MF && M <= 32;
     static constexpr int XR = MF ? 1 : M;             // rows of x staged in LDS
     static constexpr int CR = FACT ? M : 1;           // rows of slice sums
 };
@@ -83,7 +94,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     // (in bounds) and are never stored.
     using Cfg = GemvCfg<BITS, M>;
     constexpr int U = kGemvU, T = Cfg::T, PW = Cfg::PW;
-    constexpr bool FACT = Cfg::FACT, MF = Cfg::MF;
+    constexpr bool FACT = Cfg::FACT, MF = Cfg::MF, MFF = Cfg::MFF;
     constexpr int NT = WAVES * 64;
     static_assert(!MF || M == 16 || M == 32 || M == 64, "the matrix-core form holds 16, 32 or 64 rows");
     constexpr int MB = Cfg::MB;
@@ -231,8 +242,18 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         float acc[M][T];                 // factored form: sums of x * code of the open segment
         float bo[M], sx[M];              // ... and the segment's sums of x * offset and of x
         DqConst<BF> kq[T];               // dequant form: the open segment's scale and zero-point
+        // matrix-core factored form: the open segment's sums of A x code and
+        // of A (row sums, the same in every column of a block)
+        float4_t accg[MFF ? MB : 1][MFF ? T : 1], rsum[MFF ? MB : 1];
         auto open = [&]() {
-            if constexpr (FACT) {
+            if constexpr (MFF) {
+#pragma unroll
+                for (int b = 0; b < MB; ++b) {
+                    rsum[b] = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int t = 0; t < T; ++t) accg[b][t] = float4_t{0.f, 0.f, 0.f, 0.f};
+                }
+            } else if constexpr (FACT) {
 #pragma unroll
                 for (int m = 0; m < M; ++m) {
                     bo[m] = 0.f;
@@ -247,9 +268,25 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                 for (int t = 0; t < T; ++t) kq[t] = make_dq_const<BF>(sp[t], zp[t]);
             }
         };
-        // close the open segment: y += s * (acc - bo - z * sx)
+        // close the open segment: y += s * (acc - bo - z * sx); matrix-core
+        // factored form: y += s * (acc - (o + z) * (row sum of A)), o the
+        // codes' offset
         auto close = [&]() {
-            if constexpr (FACT) {
+            if constexpr (MFF) {
+                const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
+                const uint8_t* zp = zbytes + gl * PW + c * T;
+                constexpr float off = BF ? (BITS == 4 ? 128.f : 0.f) : 1024.f;
+#pragma unroll
+                for (int t = 0; t < T; ++t) {
+                    const float zo = off + (float)zp[t];
+                    const float sf = scale_f32<BF>(sp[t]);
+#pragma unroll
+                    for (int b = 0; b < MB; ++b)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            macc[b][t][q] = fmaf(sf, fmaf(-zo, rsum[b][q], accg[b][t][q]), macc[b][t][q]);
+                }
+            } else if constexpr (FACT) {
                 const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
                 const uint8_t* zp = zbytes + gl * PW + c * T;
 #pragma unroll
@@ -263,7 +300,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
             }
         };
 
-        if constexpr (FACT || SEG > 0) open();
+        if constexpr (FACT || MFF || SEG > 0) open();
 #pragma unroll
         for (int i = 0; i < U; ++i) {
             const int j = r * U + i;      // atom of the run
@@ -279,8 +316,15 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                     aring[b][i % D] = load_afrag(b, j + D);
                 }
             }
+            if constexpr (MFF) {
+                // row sums of this atom's A, by the matrix core against ones
+                const uint32_t one2 = BF ? 0x3F803F80u : 0x3C003C00u;
+                const u32x4 ones = {one2, one2, one2, one2};
+#pragma unroll
+                for (int b = 0; b < MB; ++b) rsum[b] = mfma16<BF>(afrag[b], ones, rsum[b]);
+            }
             // dequant form, group size known at run time: this atom's metadata
-            if constexpr (!FACT && SEG == 0) open();
+            if constexpr (!FACT && !MFF && SEG == 0) open();
             u32x4 xv[Cfg::XR];
             if constexpr (!MF) {
 #pragma unroll
@@ -299,6 +343,27 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 #pragma unroll
             for (int t = 0; t < T; ++t) {
                 uint32_t P[4];
+                if constexpr (MFF) {
+                    // the codes as exact 16-bit integers o + q: fp16 1024 + q,
+                    // bf16 128 + q (4-bit) or q (8-bit, converted)
+                    if constexpr (BITS == 4) {
+                        w4_code_pairs(wd[t], magic, P);
+                    } else if constexpr (BF) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const uint32_t wq = wd[2 * t + q / 2];
+                            const bf16x2_t v = {(__bf16)byte_f32(wq, 2 * (q & 1)), (__bf16)byte_f32(wq, 2 * (q & 1) + 1)};
+                            P[q] = __builtin_bit_cast(uint32_t, v);
+                        }
+                    } else {
+                        w8_code_pairs(wd[2 * t], P);
+                        w8_code_pairs(wd[2 * t + 1], P + 2);
+                    }
+                    const u32x4 pv = {P[0], P[1], P[2], P[3]};
+#pragma unroll
+                    for (int b = 0; b < MB; ++b) accg[b][t] = mfma16<BF>(afrag[b], pv, accg[b][t]);
+                    continue;
+                }
                 if constexpr (FACT) {
                     if constexpr (BF && BITS == 4) {
                         w4_code_pairs(wd[t], magic, P);          // rows (2q, 2q+1) as 128 + q
@@ -353,7 +418,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                         ++gl;
                         pos = 0;
                     }
-                    if constexpr (FACT || SEG > 0) open();
+                    if constexpr (FACT || MFF || SEG > 0) open();
                 }
             }
         }

@@ -11,9 +11,10 @@ Bars:
     output's own bfloat16 rounding is at most 2^-8 of the element; the fp32
     sums add far less than 1e-4 of the largest output, while one dropped K
     term is about max / sqrt(K)).  ref is the same oracle for the kernels
-    that round each weight to BF16 before the multiply (matrix cores, and the
-    GEMV from 5 rows); the GEMV's factored form (up to 4 rows) applies the
-    scale to a group's sum and never rounds a weight, so its ref is the exact
+    that round each weight to BF16 before the multiply (tiled GEMMs, the
+    64-slot streaming form, the GEMV from 5 rows); the factored forms (GEMV up
+    to 4 rows, streaming matrix-core form up to 32 rows) apply the scale to a
+    group's sums and never round a weight, so their ref is the exact
     contraction (Eq. 2 in float64 with the BF16 inputs);
   * integer invariant (s = 1, z = 0, integer activations): bit-exact against
     RNE_bf16 of the exact integer matmul;
@@ -95,9 +96,10 @@ def ref(d, x_bits=None, cols=None, exact=False):
 
 
 def factored(kind, M):
-    """Whether the call runs the GEMV's factored form (decode GEMV up to 4
-    rows; the GEMM entry hands up to 3 rows to the GEMV)."""
-    return M <= 4 if kind == "gemv" else M <= 3
+    """Whether the call runs a factored form that never rounds a weight: the
+    decode GEMV up to 4 rows; through the GEMM entry, the GEMV (up to 3 rows)
+    and the matrix-core streaming form with 16 or 32 row slots (up to 32)."""
+    return M <= 4 if kind == "gemv" else M <= 32
 
 
 def check(got, d, kind, what, cols=None):
