@@ -260,28 +260,44 @@ def context(torch):
                       "read+write_GB/s": round(2 * nbytes / us / 1e3, 1)}), flush=True)
 
 
-def mlp(torch, tf, make_inputs, Ms=(1, 16, 256, 2048, 8192)):
+def mlp(torch, tf, make_inputs, Ms=(1, 16, 256, 2048, 8192), dtypes=("f16", "bf16")):
     """A Llama-3-8B MLP layer (hidden 4096, intermediate 14336) around the fused
     matmul: one W4A16 GEMM for gate and up (weights concatenated along N,
     N = 28672), tf_silu_mul, one W4A16 GEMM for down (K = 14336); synthetic
     weights, G = 128.  Each stage and the whole layer timed by HIP-graph
     replay (weights used in place: 4 bytes per parameter less than fp16, and
     the 90 MB of packed weights partly stay in the 256 MB MALL across
-    replays)."""
+    replays).  Runs with fp16 and with BF16 activations and scales."""
+    from paper_2606_11357_amd.synth import make_inputs_bf16
     dev = torch.device("cuda:0")
     up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
     H, I = 4096, 14336
-    gu = make_inputs(4, max(Ms), H, 2 * I, group=GROUP, seed=0)
-    dn = make_inputs(4, 1, I, H, group=GROUP, seed=1)
-    p_gu = tf.pack_w4(up(gu["qweight"]), up(gu["qzeros"]), up(gu["s"]), H, 2 * I, GROUP)
-    p_dn = tf.pack_w4(up(dn["qweight"]), up(dn["qzeros"]), up(dn["s"]), I, H, GROUP)
-    xall = up(gu["x"])
-    del gu, dn
+    for dt in dtypes:
+        if dt == "bf16":
+            gu = make_inputs_bf16(4, max(Ms), H, 2 * I, group=GROUP, seed=0)
+            dn = make_inputs_bf16(4, 1, I, H, group=GROUP, seed=1)
+            s_gu, s_dn = up(gu["s_bits"].view(np.int16)), up(dn["s_bits"].view(np.int16))
+            xall = up(gu["x_bits"].view(np.int16)).view(torch.bfloat16)
+        else:
+            gu = make_inputs(4, max(Ms), H, 2 * I, group=GROUP, seed=0)
+            dn = make_inputs(4, 1, I, H, group=GROUP, seed=1)
+            s_gu, s_dn = up(gu["s"]), up(dn["s"])
+            xall = up(gu["x"])
+        p_gu = tf.pack_w4(up(gu["qweight"]), up(gu["qzeros"]), s_gu, H, 2 * I, GROUP)
+        p_dn = tf.pack_w4(up(dn["qweight"]), up(dn["qzeros"]), s_dn, I, H, GROUP)
+        del gu, dn, s_gu, s_dn
+        mlp_layers(torch, tf, Ms, dt, xall, p_gu, p_dn, H, I)
+        del xall, p_gu, p_dn
+        torch.cuda.empty_cache()
+
+
+def mlp_layers(torch, tf, Ms, dt, xall, p_gu, p_dn, H, I):
+    dev = xall.device
     for M in Ms:
         x = xall[:M]
-        g = torch.empty((M, 2 * I), dtype=torch.float16, device=dev)
-        h = torch.empty((M, I), dtype=torch.float16, device=dev)
-        y = torch.empty((M, H), dtype=torch.float16, device=dev)
+        g = torch.empty((M, 2 * I), dtype=x.dtype, device=dev)
+        h = torch.empty((M, I), dtype=x.dtype, device=dev)
+        y = torch.empty((M, H), dtype=x.dtype, device=dev)
         gemm_or_gemv = tf.w4a16_gemv if M <= tf.GEMV_MAX_M else tf.w4a16_gemm
         s1 = lambda i: gemm_or_gemv(x, p_gu, H, 2 * I, GROUP, out=g)
         s2 = lambda i: tf.silu_mul(g, out=h)
@@ -294,7 +310,7 @@ def mlp(torch, tf, make_inputs, Ms=(1, 16, 256, 2048, 8192)):
         flops = 2.0 * M * (H * 2 * I + I * H)
         reps = int(max(4, min(50, 5e-3 / max(flops / 1.0e15, 8e-6))))
         t = [graph_time_us(torch, f, reps) for f in (s1, s2, s3, layer)]
-        print(json.dumps({"workload": "llama3_8b_mlp_w4a16", "M": M, "hidden": H, "intermediate": I,
+        print(json.dumps({"workload": "llama3_8b_mlp_w4a16", "dtype": dt, "M": M, "hidden": H, "intermediate": I,
                           "entry": "gemv" if M <= tf.GEMV_MAX_M else "gemm",
                           "us_gate_up": round(t[0], 3), "us_silu_mul": round(t[1], 3),
                           "us_down": round(t[2], 3), "us_layer": round(t[3], 3),

@@ -221,6 +221,8 @@ int tf_dequant(int bits, const void* packed, int64_t K, int64_t N, int group,
  * aligned pointers; H must not overlap GU.
  */
 int tf_silu_mul(const uint16_t* GU_f16, int64_t M, int64_t N, uint16_t* H_f16, void* stream);
+/* The same with bfloat16 GU and H (the layer composite in the paper's dtype). */
+int tf_silu_mul_bf16(const uint16_t* GU_bf16, int64_t M, int64_t N, uint16_t* H_bf16, void* stream);
 
 #ifdef __cplusplus
 }

@@ -15,7 +15,7 @@ from .awq_oracle import (  # noqa: F401
     w8a16,
     w8a16_sym,
 )
-from .mlp_oracle import mlp_w4a16, silu, silu_mul  # noqa: F401
+from .mlp_oracle import mlp_w4a16, mlp_w4a16_bf16, silu, silu_mul  # noqa: F401
 from .bf16_oracle import (  # noqa: F401
     bf16_decode,
     bf16_encode,

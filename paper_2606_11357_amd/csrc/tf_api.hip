@@ -70,6 +70,13 @@ int gemv_entry(int bits, const uint16_t* A, const void* packed, uint16_t* C, int
     return tf::launch_gemv(L, A, packed, C, M, ws, static_cast<hipStream_t>(stream), bf);
 }
 
+int silu_mul_entry(const uint16_t* GU, int64_t M, int64_t N, uint16_t* H, void* stream, bool bf) {
+    if (!GU || !H) return TF_ERR_NULL;
+    if (M < 1 || M > TF_MAX_M || N <= 0 || N > TF_MAX_DIM || N % 8 != 0) return TF_ERR_SHAPE;
+    if (misaligned(GU) || misaligned(H)) return TF_ERR_ALIGN;
+    return tf::launch_silu_mul(GU, M, N, H, static_cast<hipStream_t>(stream), bf);
+}
+
 }  // namespace
 
 extern "C" {
@@ -212,10 +219,11 @@ int tf_dequant(int bits, const void* packed, int64_t K, int64_t N, int group, in
 }
 
 int tf_silu_mul(const uint16_t* GU_f16, int64_t M, int64_t N, uint16_t* H_f16, void* stream) {
-    if (!GU_f16 || !H_f16) return TF_ERR_NULL;
-    if (M < 1 || M > TF_MAX_M || N <= 0 || N > TF_MAX_DIM || N % 8 != 0) return TF_ERR_SHAPE;
-    if (misaligned(GU_f16) || misaligned(H_f16)) return TF_ERR_ALIGN;
-    return tf::launch_silu_mul(GU_f16, M, N, H_f16, static_cast<hipStream_t>(stream));
+    return silu_mul_entry(GU_f16, M, N, H_f16, stream, false);
+}
+
+int tf_silu_mul_bf16(const uint16_t* GU_bf16, int64_t M, int64_t N, uint16_t* H_bf16, void* stream) {
+    return silu_mul_entry(GU_bf16, M, N, H_bf16, stream, true);
 }
 
 }  // extern "C"

@@ -514,5 +514,5 @@ int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16
                    void* ws, size_t ws_bytes, hipStream_t s, bool bf);
 int launch_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, size_t ws_bytes, hipStream_t s, bool bf);
-int launch_silu_mul(const uint16_t* gu, int64_t M, int64_t N, uint16_t* h, hipStream_t s);
+int launch_silu_mul(const uint16_t* gu, int64_t M, int64_t N, uint16_t* h, hipStream_t s, bool bf);
 }  // namespace tf

@@ -29,7 +29,7 @@ EXPORTS = (
     "tf_layout_version", "tf_status_str", "tf_packed_bytes", "tf_pack_w4", "tf_pack_w8",
     "tf_pack_w8_sym", "tf_workspace_bytes", "tf_w4a16_gemm", "tf_w8a16_gemm", "tf_w4a16_gemv",
     "tf_w8a16_gemv", "tf_w4a16_gemm_bf16", "tf_w8a16_gemm_bf16", "tf_w4a16_gemv_bf16",
-    "tf_w8a16_gemv_bf16", "tf_unpack", "tf_dequant", "tf_silu_mul",
+    "tf_w8a16_gemv_bf16", "tf_unpack", "tf_dequant", "tf_silu_mul", "tf_silu_mul_bf16",
 )
 
 
@@ -71,6 +71,7 @@ def load() -> ctypes.CDLL:
         "tf_unpack": (I, [I, P, I64, I64, I, P, P, P]),
         "tf_dequant": (I, [I, P, I64, I64, I, I, P, P]),
         "tf_silu_mul": (I, [P, I64, I64, P, P]),
+        "tf_silu_mul_bf16": (I, [P, I64, I64, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -253,14 +254,17 @@ def dequant(bits: int, packed, K: int, N: int, group: int = 128, dtype=None):
 
 
 def silu_mul(gu, out=None):
-    """H = silu(gu[:, :N]) * gu[:, N:] for an fp16 [M, 2N] CUDA tensor (the gate
-    and up halves side by side); returns fp16 [M, N]."""
+    """H = silu(gu[:, :N]) * gu[:, N:] for an fp16 or bfloat16 [M, 2N] CUDA
+    tensor (the gate and up halves side by side); returns [M, N] of gu's dtype."""
     torch = _torch()
     _need_cuda(gu, out)
-    if gu.dtype != torch.float16 or gu.dim() != 2 or gu.shape[1] % 2 != 0:
-        raise ValueError("gu must be fp16 [M, 2N]")
+    if gu.dtype not in (torch.float16, torch.bfloat16) or gu.dim() != 2 or gu.shape[1] % 2 != 0:
+        raise ValueError("gu must be fp16 or bf16 [M, 2N]")
     M, N = gu.shape[0], gu.shape[1] // 2
     if out is None:
-        out = torch.empty((M, N), dtype=torch.float16, device=gu.device)
-    _check(load().tf_silu_mul(_ptr(gu), M, N, _ptr(out), _stream(gu.device)), "tf_silu_mul")
+        out = torch.empty((M, N), dtype=gu.dtype, device=gu.device)
+    elif out.dtype != gu.dtype:
+        raise ValueError("out must have gu's dtype")
+    name = "tf_silu_mul_bf16" if gu.dtype == torch.bfloat16 else "tf_silu_mul"
+    _check(getattr(load(), name)(_ptr(gu), M, N, _ptr(out), _stream(gu.device)), name)
     return out

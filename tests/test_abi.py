@@ -217,3 +217,4 @@ def test_binding_refuses_cpu_tensors():
     ((P, 4, 64, P_ODD, NULL), tfb.TF_ERR_ALIGN)])
 def test_silu_mul_rejects(lib, args, want):
     assert lib.tf_silu_mul(*args) == want
+    assert lib.tf_silu_mul_bf16(*args) == want

@@ -8,7 +8,7 @@ from __future__ import annotations
 import numpy as np
 import pytest
 
-from paper_2606_11357_amd.synth import make_inputs
+from paper_2606_11357_amd.synth import make_inputs, make_inputs_bf16
 
 from test_gpu_parity import dev, pack, tf  # noqa: F401
 
@@ -18,18 +18,32 @@ pytestmark = pytest.mark.gpu
 CASES = [("gemm", 4, 1100, 1024, 2320),   # 256-row tiles, stream-K
          ("gemm", 8, 300, 4096, 1024),    # 128-row tiles, split-K
          ("gemm", 4, 40, 4096, 1024),     # streaming matrix-core form, 64 row slots
+         ("gemm", 4, 20, 14336, 4096),    # streaming matrix-core form, factored, K split
          ("gemv", 4, 1, 14336, 4096),     # decode GEMV, K split
          ("gemv", 8, 5, 4096, 520)]
 
 
-def test_graph_replays_match_eager(tf):
+def _inputs(tf, dt, bits, M, K, N, seed):
+    """x and the packed weight for fp16 or BF16 calls (BF16 scales packed as their bits)."""
+    if dt == "f16":
+        d = make_inputs(bits, M, K, N, seed=seed)
+        return dev(d["x"]), pack(tf, d)
+    d = make_inputs_bf16(bits, M, K, N, seed=seed)
+    s = dev(d["s_bits"].view(np.int16))
+    p = (tf.pack_w4(dev(d["qweight"]), dev(d["qzeros"]), s, K, N, 128) if bits == 4
+         else tf.pack_w8(dev(d["qweight"]), dev(d["zeros"]), s, K, N, 128))
+    return dev(d["x_bits"].view(np.int16)).view(torch.bfloat16), p
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+def test_graph_replays_match_eager(tf, dt):
     ws = torch.zeros(max(tf.workspace_bytes(b, m, k, n) for _, b, m, k, n in CASES), dtype=torch.uint8,
                      device="cuda")
     calls = []
     for i, (kind, bits, M, K, N) in enumerate(CASES):
-        d = make_inputs(bits, M, K, N, seed=300 + i)
-        calls.append((getattr(tf, f"w{bits}a16_{kind}"), dev(d["x"]), pack(tf, d), K, N,
-                      torch.empty((M, N), dtype=torch.float16, device="cuda")))
+        x, p = _inputs(tf, dt, bits, M, K, N, 300 + i)
+        calls.append((getattr(tf, f"w{bits}a16_{kind}"), x, p, K, N,
+                      torch.empty((M, N), dtype=x.dtype, device="cuda")))
 
     def run_all():
         for fn, x, p, K, N, out in calls:
@@ -49,5 +63,5 @@ def test_graph_replays_match_eager(tf):
         g.replay()
         torch.cuda.synchronize()
         for (kind, bits, M, K, N), e, (*_, out) in zip(CASES, eager, calls):
-            np.testing.assert_array_equal(out.cpu().numpy().view(np.uint16), e.cpu().numpy().view(np.uint16),
-                                          err_msg=f"replay {rep}: {kind} W{bits} {M}x{K}x{N}")
+            np.testing.assert_array_equal(out.view(torch.int16).cpu().numpy(), e.view(torch.int16).cpu().numpy(),
+                                          err_msg=f"replay {rep}: {dt} {kind} W{bits} {M}x{K}x{N}")

@@ -75,3 +75,67 @@ def test_mlp_llama3_8b_sampled(tf):
     want = oracle.mlp_w4a16(gu["x"][rows], gu["qweight"], gu["qzeros"], gu["s"],
                             dn["qweight"], dn["qzeros"], dn["s"], 128)
     assert_parity(got[rows], want, "Llama-3-8B MLP sampled rows")
+
+
+# ---------------------------------------------------------------------------
+# the composite in BF16 (the paper's dtype)
+# ---------------------------------------------------------------------------
+def _bf16_dev(bits):
+    return dev(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16)
+
+
+def _bf16_bits(t):
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def bf16_ulps(a, b):
+    """|a - b| in bfloat16 units in the last place (finite patterns)."""
+    ia, ib = a.astype(np.int32), b.astype(np.int32)
+    ia = np.where(ia >= 0x8000, 0x8000 - ia, ia)
+    ib = np.where(ib >= 0x8000, 0x8000 - ib, ib)
+    return np.abs(ia - ib)
+
+
+@pytest.mark.parametrize("M,N", [(1, 8), (7, 136), (64, 4096), (33, 14336)])
+def test_silu_mul_bf16_vs_oracle(tf, M, N):
+    """fp32 on the GPU against float64 on the host, both rounded to bfloat16
+    once: at most one ulp apart.  Gates stay above -88, where the fp32
+    exponential of -g is finite (below, the GPU returns -0 for a product that
+    is a bfloat16 subnormal at most)."""
+    rng = np.random.default_rng(M * N + 1)
+    v = (rng.standard_normal((M, 2 * N)) * 5.0).astype(np.float32)
+    v[0, :4] = np.array([0.0, 1e30, -1e30, -20.0], dtype=np.float32)
+    bits = (v.view(np.uint32) >> 16).astype(np.uint16)
+    got = _bf16_bits(tf.silu_mul(_bf16_dev(bits)))
+    want = oracle.bf16_encode(oracle.to_bf16(oracle.silu_mul(oracle.bf16_decode(bits))))
+    ulps = bf16_ulps(got, want)
+    assert ulps.max() <= 1, (M, N, ulps.max())
+
+
+def _mlp_inputs_bf16(M, K, I, seed):
+    from paper_2606_11357_amd.synth import make_inputs_bf16
+    return make_inputs_bf16(4, M, K, 2 * I, seed=seed), make_inputs_bf16(4, 1, I, K, seed=seed + 1)
+
+
+def _pack_bf16(tf, d):
+    return tf.pack_w4(dev(d["qweight"]), dev(d["qzeros"]), dev(d["s_bits"].view(np.int16)),
+                      d["K"], d["N"], d["group"])
+
+
+@pytest.mark.parametrize("M,K,I", [(64, 512, 1024), (5, 1024, 512), (200, 256, 2048)])
+def test_mlp_composite_bf16_parity(tf, M, K, I):
+    """gate/up GEMM -> silu * up -> down GEMM in BF16 against the BF16 oracle
+    composite, to the stated tolerance (a stored bfloat16 intermediate may
+    round one ulp apart on the two sides, so no per-element bound)."""
+    gu, dn = _mlp_inputs_bf16(M, K, I, seed=M + I + 7)
+    x = _bf16_dev(gu["x_bits"])
+    g = tf.w4a16_gemm(x, _pack_bf16(tf, gu), K, 2 * I, 128)
+    h = tf.silu_mul(g)
+    y = tf.w4a16_gemm(h, _pack_bf16(tf, dn), I, K, 128)
+    torch.cuda.synchronize()
+    got = oracle.bf16_decode(_bf16_bits(y))
+    want = oracle.mlp_w4a16_bf16(gu["x_bits"], gu["qweight"], gu["qzeros"], gu["s_bits"],
+                                 dn["qweight"], dn["qzeros"], dn["s_bits"], 128)
+    scale = np.abs(want).max()
+    err = np.abs(got - want).max()
+    assert np.all(np.isfinite(got)) and err <= 1e-2 * scale, (M, K, I, err / scale)

@@ -69,6 +69,29 @@ def test_composite_definition():
     np.testing.assert_allclose(y, want, rtol=1e-12, atol=1e-9)
 
 
+def test_composite_definition_bf16():
+    """The BF16 composite with unit scales and zero zero-points: integer
+    matmuls around the gate, GU and H rounded to bfloat16 by the exact
+    rational rounding of the BF16 pins (not the oracle's own rounding)."""
+    from fractions import Fraction
+    from test_oracle_pins_bf16 import bf16_value, rne_bf16_bits
+    rng = np.random.default_rng(1)
+    M, K, I, G = 3, 64, 32, 32
+    xi = rng.integers(-2, 3, size=(M, K))
+    qgu = rng.integers(0, 4, size=(K, 2 * I)).astype(np.uint8)
+    qd = rng.integers(0, 4, size=(I, 8)).astype(np.uint8)
+    x_bits = (xi.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    z = lambda r, n: np.zeros((r, n), np.uint8)
+    one = lambda r, n: np.full((r, n), 0x3F80, np.uint16)
+    y = oracle.mlp_w4a16_bf16(x_bits, pack_nibbles(qgu), pack_nibbles(z(K // G, 2 * I)), one(K // G, 2 * I),
+                              pack_nibbles(qd), pack_nibbles(z(I // G, 8)), one(I // G, 8), G)
+    rnd = np.vectorize(lambda v: float(bf16_value(rne_bf16_bits(Fraction(float(v))))))
+    gu = rnd((xi.astype(np.int64) @ qgu.astype(np.int64)).astype(np.float64))
+    h = rnd(gu[:, :I] / (1.0 + np.exp(-gu[:, :I])) * gu[:, I:])
+    want = h @ qd.astype(np.float64)
+    np.testing.assert_allclose(y, want, rtol=1e-12, atol=1e-9)
+
+
 def _mut_sigmoid_only(g):            # the gate without the factor g
     return 1.0 / (1.0 + np.exp(-np.asarray(g, np.float64)))
 
