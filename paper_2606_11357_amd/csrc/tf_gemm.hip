@@ -21,9 +21,12 @@
 //    which then stay in that XCD's L2.
 //  - When the tiles are too few to occupy the device and a workspace is
 //    given, each tile's K is cut into S slices of whole chunks, one workgroup
-//    each; a slice parks its fp32 partial tile in the workspace and the last
-//    slice of a tile to arrive adds all of them in slice order (bitwise
-//    reproducible) and writes C.
+//    each; every slice parks its fp32 partial tile in the workspace, and a
+//    second launch on the same stream (splitk_reduce_kernel) adds the slices
+//    of every tile in slice order (bitwise reproducible) and writes C, spread
+//    over all compute units.  (Letting the last slice of each tile do that
+//    sum left one workgroup per tile streaming S - 1 partial tiles, one
+//    latency-bound row block at a time, while the rest of the GPU idled.)
 #include "tf_internal.h"
 
 #include <algorithm>
@@ -45,15 +48,15 @@ __device__ __forceinline__ int a_slot(int row, int ch) { return lds_a_slot(row, 
 
 // MPC: metadata groups per chunk (1 when a group spans the whole chunk, else
 // chunk rows / group); the group of step j is j / (chunk steps / MPC).
-// Most K slices per tile (the finishing slice holds the other slices' parts
-// of one row block in registers).
-constexpr int kMaxSplit = 4;
+// Most K slices per tile (measured on MI355X over the split shapes of the
+// M = 256..768 MLP sweep and W8 K = N = 4096: 8 beats 4 where K is long and
+// the tiles few, and ties elsewhere; 2 and 1 lose everywhere).
+constexpr int kMaxSplit = 8;
 
 // Split-K arguments: S slices per tile of cps chunks each (S = 1: no split);
-// arrival counters (zero at rest) and partial tiles in the workspace.
+// the partial tiles in the workspace.
 struct SplitK {
     int S, cps;
-    uint32_t* cnt;
     float* part;
 };
 
@@ -272,56 +275,48 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
         return;
     }
     // Park this slice's partial tile (wave w's 128 x 64 part, block (i, t) as
-    // 64 consecutive float4, one per lane) with device-coherent stores; wait
-    // for them to complete before counting the arrival.
-    constexpr uint32_t kWavePart = kBM * 64 * 4;              // bytes of a wave's part
-    auto part_rsrc = [&](int sl) {
-        return make_rsrc(sk.part + ((int64_t)tile * sk.S + sl) * (kBM * kBN) + wave * (kBM * 64), kWavePart);
-    };
+    // 64 consecutive float4, one per lane); splitk_reduce_kernel, launched
+    // next on the same stream, adds the slices.
     {
-        const __amdgpu_buffer_rsrc_t pr = part_rsrc(split);
+        const __amdgpu_buffer_rsrc_t pr =
+            make_rsrc(sk.part + ((int64_t)tile * sk.S + split) * (kBM * kBN) + wave * (kBM * 64), kBM * 64 * 4);
 #pragma unroll
         for (int i = 0; i < 8; ++i)
 #pragma unroll
             for (int t = 0; t < 4; ++t)
                 __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, acc[i][t]), pr,
-                                                       (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, kSc1);
+                                                       (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, 0);
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    __shared__ int last;
-    if (tid == 0)
-        last = __hip_atomic_fetch_add(&sk.cnt[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-               (uint32_t)(sk.S - 1);
-    __syncthreads();
-    if (!last) return;
-    // The last slice adds the tile's slices in order: those before it, its
-    // own from registers, those after it.  The other slices' parts of one row
-    // block are all requested before any is used, so the block costs one
-    // memory latency, not one per (slice, column block).
+}
+
+// Split-K reduction: one thread per float4 of a tile's parked partial (the
+// main kernel's layout: wave part w of kBM x 64 floats, block (i, t) as 64
+// consecutive float4, lane (c, kg) holding rows 16 i + 4 kg + 0..3 of column
+// 16 t + c), summed over the S slices in slice order; the four outputs are
+// rounded once.  Consecutive threads read consecutive float4.
+template <bool BF>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float4_t* __restrict__ part,
+                                                            uint16_t* __restrict__ C, int M, int N,
+                                                            int tiles_n, int S, int64_t total) {
+    constexpr int kPerTile = kBM * kBN / 4;        // float4 per slice of one tile
+    constexpr int kPerWave = kBM * 64 / 4;         // float4 per wave part
+    const int64_t f = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (f >= total) return;
+    const int64_t tile = f / kPerTile;
+    const int e = (int)(f - tile * kPerTile);
+    const int w = e / kPerWave, rem = e - w * kPerWave;
+    const int blk = rem >> 6, lane = rem & 63;
+    const int i = blk >> 2, t = blk & 3, c = lane & 15, kg = lane >> 4;
+    const float4_t* p = part + tile * S * kPerTile + e;
+    float4_t r = p[0];
+    for (int sl = 1; sl < S; ++sl) r += p[(int64_t)sl * kPerTile];
+    const int64_t tm = tile / tiles_n, tn = tile - tm * tiles_n;
+    const int64_t col = tn * kBN + w * 64 + 16 * t + c;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        float4_t p[kMaxSplit][4];
-#pragma unroll
-        for (int sl = 0; sl < kMaxSplit; ++sl)
-            if (sl < sk.S && sl != split) {
-                const __amdgpu_buffer_rsrc_t pr = part_rsrc(sl);
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    p[sl][t] = __builtin_bit_cast(float4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                                                pr, (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, kSc1));
-            }
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            float4_t r = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int sl = 0; sl < kMaxSplit; ++sl)
-                if (sl < sk.S) r += sl == split ? acc[i][t] : p[sl][t];
-            store_block(i, t, r);
-        }
+    for (int q = 0; q < 4; ++q) {
+        const int64_t row = tm * kBM + 16 * i + 4 * kg + q;
+        if (row < M && col < N) C[row * N + col] = round_out<BF>(r[q]);
     }
-    if (tid == 0)   // leave the counter at zero for the next call
-        __hip_atomic_store(&sk.cnt[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Generic kernel for the cases the main one leaves out (K not a multiple of
@@ -449,8 +444,9 @@ SplitPlan plan_split(const Layout& L, int64_t M) {
     return {(chunks + cps - 1) / cps, cps};    // no empty slice
 }
 
-// Workspace of a split plan: arrival counters (one per tile, fixed region),
-// then one fp32 partial tile per (tile, slice).
+// Workspace of a split plan: the shared counter region at offset 0 (the
+// other kernels' arrival counters; this one leaves it untouched), then one
+// fp32 partial tile per (tile, slice).
 int64_t split_workspace_bytes(const Layout& L, int64_t M, const SplitPlan& sp) {
     if (sp.S <= 1) return 0;
     const int64_t tiles = ((M + kBM - 1) / kBM) * ((L.N + kBN - 1) / kBN);
@@ -470,14 +466,15 @@ int launch_main(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t*
     const int gshift = __builtin_ctz((unsigned)L.group);
     SplitPlan sp = plan_split<BITS>(L, M);
     if (!ws) sp = {1, (int)(L.K / (kBK * chunk_steps<BITS>()))};
-    SplitK sk{sp.S, sp.cps, nullptr, nullptr};
-    if (sp.S > 1) {
-        sk.cnt = static_cast<uint32_t*>(ws);
-        sk.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes);
-    }
-    return launch(gemm_kernel<BITS, MPC, BF>, dim3((unsigned)(tiles_m * tiles_n * sp.S)), dim3(kGemmThreads),
-                  0, s, A, pk, C, (int)M, (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na,
-                  (int)L.ng, (int)L.np, tiles_m, tiles_n, sk);
+    SplitK sk{sp.S, sp.cps, nullptr};
+    if (sp.S > 1) sk.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes);
+    const int rc = launch(gemm_kernel<BITS, MPC, BF>, dim3((unsigned)(tiles_m * tiles_n * sp.S)),
+                          dim3(kGemmThreads), 0, s, A, pk, C, (int)M, (int)L.K, (int)L.N, gshift, L.s_off,
+                          L.z_off, (int)L.na, (int)L.ng, (int)L.np, tiles_m, tiles_n, sk);
+    if (rc || sp.S == 1) return rc;
+    const int64_t total = (int64_t)tiles_m * tiles_n * (kBM * kBN / 4);
+    return launch(splitk_reduce_kernel<BF>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                  reinterpret_cast<const float4_t*>(sk.part), C, (int)M, (int)L.N, tiles_n, sp.S, total);
 }
 
 template <int BITS, bool BF>

@@ -263,7 +263,9 @@ def test_workspace_shared_across_shapes(tf):
                                            (8, 512, 4096, 4096, 128), (4, 100, 4096, 3000, 128),
                                            (4, 300, 2048, 520, 64), (8, 40, 8192, 264, 32),
                                            (4, 700, 1536, 1000, 128), (4, 64, 8192, 1024, 128),
-                                           (8, 40, 4096, 4096, 128)])
+                                           (8, 40, 4096, 4096, 128),
+                                           # 8 and 7 K slices (12 and 37 tiles of 128 x 256)
+                                           (4, 100, 4096, 9400, 128)])
 def test_gemm_workspace_modes(tf, bits, M, K, N, G):
     """The K-split kernels (workspace: stream-K for 256-row tiles, split-K for
     128-row tiles) and the whole-tile kernels (no workspace) both meet the
