@@ -96,20 +96,18 @@ __device__ __forceinline__ void barrier_after_a_loads() {
 // per block; a block walks its range tile by tile, so a tile may be computed
 // in several K segments by consecutive blocks.  Every segment of a split
 // tile parks its fp32 partial tile in the workspace (slot 2v for the first
-// segment of block v's range, 2v + 1 for its last) and counts its arrival on
-// the counter of the tile's first block; the last to arrive adds all
-// partials in K order (so the result does not depend on which block came
-// last), writes C and returns the counter to zero.  Partials and counters are
-// accessed with device-coherent (sc1) loads and stores: the blocks of one
-// tile run on different XCDs, whose L2 caches are not coherent.
-// Other segments whose partial row block the finishing block holds in
-// registers at once.
+// segment of block v's range, 2v + 1 for its last), and a second launch on
+// the same stream (stream_k_reduce_kernel, spread over all compute units)
+// adds each split tile's segments in K order and writes C; the kernel
+// boundary orders the parked stores before those loads on every XCD.
+// (Summing in the last segment to arrive left one block per tile streaming
+// the other parts while the rest of the GPU idled.)
+// Most further segments per split tile the hybrid schedule accepts.
 constexpr int kMaxParts = 3;
 
 struct StreamK {
     int groups;               // G, 0 = data-parallel
     int units;                // tiles * chunks
-    uint32_t* cnt;            // G arrival counters (zero at rest)
     float* part;              // 2 G partial tiles of kBM x kBN floats
     int dp_rounds;            // hybrid: whole tiles per block before the stream-K units
 };
@@ -143,7 +141,6 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     __shared__ __align__(16) u32x4 As0[kBM * kBK / 8], As1[kBM * kBK / 8], As2[kBM * kBK / 8],
         As3[kBM * kBK / 8];
     auto abuf = [&](int j) -> u32x4* { return j == 0 ? As0 : j == 1 ? As1 : j == 2 ? As2 : As3; };
-    __shared__ int last_flag;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -464,7 +461,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
             store_tile(row0, col0, whole);
         } else {
             // Park the partial: wave w's 256 x 64 part at w * 16384 floats,
-            // block (i, t) as 64 consecutive float4 (one per lane).
+            // block (i, t) as 64 consecutive float4 (one per lane); slot 2v
+            // holds this block's first segment, 2v + 1 its last.
+            // stream_k_reduce_kernel, launched next on the same stream, adds
+            // each split tile's segments.
             const int slot = 2 * v + (useg == ua ? 0 : 1);
             float* part = sk.part + (int64_t)slot * (kBM * kBN);
             const __amdgpu_buffer_rsrc_t pr = make_rsrc(part + wave * (kBM * 64), kBM * 64 * 4);
@@ -473,79 +473,59 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
 #pragma unroll
                 for (int t = 0; t < 4; ++t)
                     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, acc[i][t]), pr,
-                                                           (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, kSc1);
-            __builtin_amdgcn_s_waitcnt(0);                // this thread's partial stores have completed
-            __syncthreads();
-            const int t0 = tile * chunks - dpu;            // the tile's first unit, stream-K numbering
-            const int vlo = sk_owner(t0, G, U), vhi = sk_owner(t0 + chunks - 1, G, U);
-            if (tid == 0)
-                last_flag = __hip_atomic_fetch_add(&sk.cnt[vlo], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-                            (uint32_t)(vhi - vlo);
-            __syncthreads();
-            if (last_flag) {
-                // Sum the segments' parts in K order (block vlo first).  This
-                // block's own part is read back too (it was just parked), so
-                // the sum needs no accumulator registers; the parts of one row
-                // block are all requested before any is used (one memory
-                // latency per row block, not one per segment and column
-                // block).  More than kMaxParts + 1 segments take the
-                // one-by-one path.
-                const int nb = vhi - vlo;
-                __amdgpu_buffer_rsrc_t prs[kMaxParts + 1];     // segment vlo + j's part
-#pragma unroll
-                for (int j = 0; j <= kMaxParts; ++j) {
-                    const int w = min(vlo + j, vhi);
-                    const int sw = 2 * w + (sk_begin(w, G, U) >= t0 ? 0 : 1);
-                    prs[j] = make_rsrc(sk.part + (int64_t)sw * (kBM * kBN) + wave * (kBM * 64), kBM * 64 * 4);
-                }
-                auto part_of = [&](const __amdgpu_buffer_rsrc_t& q, int i, int t) {
-                    return __builtin_bit_cast(float4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                                            q, (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, kSc1));
-                };
-                auto total_block = [&](int i, float4_t (&blk)[4]) {
-                    if (nb <= kMaxParts) {
-                        float4_t p[kMaxParts + 1][4];
-#pragma unroll
-                        for (int j = 0; j <= kMaxParts; ++j)
-                            if (j <= nb)
-#pragma unroll
-                                for (int t = 0; t < 4; ++t) p[j][t] = part_of(prs[j], i, t);
-#pragma unroll
-                        for (int t = 0; t < 4; ++t) {
-                            float4_t r = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                            for (int j = 0; j <= kMaxParts; ++j)
-                                if (j <= nb) r += p[j][t];
-                            blk[t] = r;
-                        }
-                        return;
-                    }
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) {
-                        float4_t r = {0.f, 0.f, 0.f, 0.f};
-                        for (int w = vlo; w <= vhi; ++w) {
-                            const int sw = 2 * w + (sk_begin(w, G, U) >= t0 ? 0 : 1);
-                            r += part_of(make_rsrc(sk.part + (int64_t)sw * (kBM * kBN) + wave * (kBM * 64),
-                                                   kBM * 64 * 4), i, t);
-                        }
-                        blk[t] = r;
-                    }
-                };
-                store_tile(row0, col0, total_block);
-                if (tid == 0) __hip_atomic_store(&sk.cnt[vlo], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
+                                                           (uint32_t)(((i * 4 + t) * 64 + lane) * 16), 0, 0);
         }
     }
+}
+
+// Stream-K reduction: one thread per float4 of a split tile's parked parts
+// (the main kernel's layout: wave part w of 256 x 64 floats, block (i, t) as
+// 64 consecutive float4; lane (c, kg) holds row 16 i + c, columns
+// 16 t + 4 kg + 0..3, C transposed by the operand order), summed over the
+// tile's segments in K order (the owner of its first unit first) and
+// written as four outputs rounded once.  Tiles are the stream-K tiles after
+// the whole-tile rounds; a tile inside one block's range was stored whole.
+template <bool BF>
+__global__ __launch_bounds__(256) void stream_k_reduce_kernel(
+    const float4_t* __restrict__ part, uint16_t* __restrict__ C, int M, int N, int tiles_m,
+    int tiles_n, int col_major, int G, int U, int chunks, int tile0, int64_t total) {
+    constexpr int kPerTile = kBM * kBN / 4;        // float4 per part of one tile
+    constexpr int kPerWave = kBM * 64 / 4;         // float4 per wave part
+    const int64_t f = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (f >= total) return;
+    const int tile = tile0 + (int)(f / kPerTile);
+    const int e = (int)(f % kPerTile);
+    const int t0 = (tile - tile0) * chunks;        // the tile's first unit, stream-K numbering
+    const int vlo = sk_owner(t0, G, U), vhi = sk_owner(t0 + chunks - 1, G, U);
+    if (vlo == vhi) return;                        // one block's range: stored whole
+    float4_t r = {0.f, 0.f, 0.f, 0.f};
+    for (int w = vlo; w <= vhi; ++w) {
+        const int sw = 2 * w + (sk_begin(w, G, U) >= t0 ? 0 : 1);
+        r += part[(int64_t)sw * kPerTile + e];
+    }
+    const int wave = e / kPerWave, rem = e % kPerWave;
+    const int blk = rem >> 6, lane = rem & 63;
+    const int i = blk >> 2, t = blk & 3, c = lane & 15, kg = lane >> 4;
+    const int tm = col_major ? tile % tiles_m : tile / tiles_n;
+    const int tn = col_major ? tile / tiles_m : tile % tiles_n;
+    const int64_t m = (int64_t)tm * kBM + 16 * i + c;
+    const int64_t n = (int64_t)tn * kBN + wave * 64 + 16 * t + 4 * kg;     // N % 8 == 0
+    if (m < M && n < N)
+        *reinterpret_cast<uint2*>(C + m * N + n) = uint2{round_out2<BF>(r[0], r[1]), round_out2<BF>(r[2], r[3])};
+}
+
+// Walk the tile list along N (column-major) when the weights outweigh the
+// activations: each XCD band then covers fewer weight panels.
+int col_major_for(const Layout& L, int64_t M) {
+    const int64_t a_bytes = M * L.K * 2, w_bytes = L.total;
+    return w_bytes > a_bytes ? 1 : 0;
 }
 
 template <int BITS, int MPC, bool BF>
 int launch_mpc(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
                StreamK sk, int tiles_m, int tiles_n, hipStream_t s) {
     const int gshift = __builtin_ctz((unsigned)L.group);
-    // Walk the tile list along N (column-major) when the weights outweigh the
-    // activations: each XCD band then covers fewer weight panels.
-    const int64_t a_bytes = M * L.K * 2, w_bytes = L.total;
-    const int col_major = w_bytes > a_bytes ? 1 : 0;
+    const int col_major = col_major_for(L, M);
     const unsigned grid = sk.groups ? (unsigned)sk.groups : (unsigned)(tiles_m * tiles_n);
     return launch(gemm256_kernel<BITS, MPC, BF>, dim3(grid), dim3(kThreads), 0, s, A, pk, C, (int)M,
                   (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na, (int)L.ng, (int)L.np,
@@ -607,7 +587,7 @@ int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16
     const int tiles = tiles_m * tiles_n, chunks = (int)(L.K / (kBK * kCS));
     const int64_t need = gemm256_workspace_bytes(L, M);
     const int cus = device_cus();
-    StreamK sk{0, 0, nullptr, nullptr, 0};
+    StreamK sk{0, 0, nullptr, 0};
     // Otherwise (with a workspace) stream-K, with at least kSkMinUnits K
     // chunks per block.  With at least one full wave of tiles the full waves
     // stay whole tiles and only the tiles after them are split ("hybrid"):
@@ -625,18 +605,29 @@ int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16
         // the stream-K part keeps at least kSkMinUnits chunks per block: a
         // short remainder joins the last whole wave
         if (dp_rounds > 0 && (int64_t)(tiles - dp_rounds * G) * chunks < (int64_t)G * kSkMinUnits) --dp_rounds;
-        // and cuts each of its tiles into at most kMaxParts + 1 segments (the
-        // finishing block's fast path); otherwise everything is split
+        // and cuts each of its tiles into at most kMaxParts + 1 segments;
+        // otherwise everything is split
         if (dp_rounds > 0 && (int64_t)(tiles - dp_rounds * G) * chunks * kMaxParts < (int64_t)G * chunks)
             dp_rounds = 0;
         const int64_t units = (int64_t)(tiles - dp_rounds * G) * chunks;
         if (dp_rounds == 0) G = (int)std::min<int64_t>(G, std::max<int64_t>(1, units / kSkMinUnits));
         if (G > kXcds) G -= G % kXcds;
-        sk = StreamK{G, (int)units, static_cast<uint32_t*>(ws),
-                     reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes), dp_rounds};
+        sk = StreamK{G, (int)units, reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes),
+                     dp_rounds};
     }
-    return bf ? launch_bf<true>(L, A, pk, C, M, sk, tiles_m, tiles_n, s)
-              : launch_bf<false>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+    const int rc = bf ? launch_bf<true>(L, A, pk, C, M, sk, tiles_m, tiles_n, s)
+                      : launch_bf<false>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
+    if (rc || sk.groups == 0) return rc;
+    const int tile0 = sk.dp_rounds * sk.groups;                  // first stream-K tile
+    const int64_t total = (int64_t)(tiles - tile0) * (kBM * kBN / 4);
+    const dim3 grid((unsigned)((total + 255) / 256));
+    const float4_t* part = reinterpret_cast<const float4_t*>(sk.part);
+    const int cm = col_major_for(L, M);
+    if (bf)
+        return launch(stream_k_reduce_kernel<true>, grid, dim3(256), 0, s, part, C, (int)M, (int)L.N, tiles_m,
+                      tiles_n, cm, sk.groups, sk.units, chunks, tile0, total);
+    return launch(stream_k_reduce_kernel<false>, grid, dim3(256), 0, s, part, C, (int)M, (int)L.N, tiles_m,
+                  tiles_n, cm, sk.groups, sk.units, chunks, tile0, total);
 }
 
 bool gemm256_fills_device(const Layout& L, int64_t M) {
