@@ -233,12 +233,14 @@ def test_integer_invariant_bf16(tf, bits, kind, M, K, N):
     assert_bf16_equal(got, oracle.bf16_encode(oracle.to_bf16(exact)))
 
 
-@pytest.mark.parametrize("K,N", [(4096, 14336), (14336, 4096)])
-def test_gemm_bf16_full_size_sampled(tf, K, N):
+@pytest.mark.parametrize("M,K,N,xstd", [(2048, 4096, 14336, 1.0), (2048, 14336, 4096, 1.0),
+                                         (1024, 4096, 32768, 0.5), (1024, 32768, 8192, 0.5)])
+def test_gemm_bf16_full_size_sampled(tf, M, K, N, xstd):
     """The Llama-3-8B MLP shapes at M = 2048 in the benchmark's launch
-    configuration (default workspace): 96 sampled output columns, all rows."""
-    M, G = 2048, 128
-    d = make_inputs_bf16(4, M, K, N, group=G, seed=K + 2 * N)
+    configuration (default workspace) and the 32K-dimension shapes at
+    M = 1024: 96 sampled output columns, all rows."""
+    G = 128
+    d = make_inputs_bf16(4, M, K, N, group=G, seed=K + 2 * N, x_std=xstd)
     got = run(tf, "gemm", d, pack(tf, d))
     cols = np.sort(np.random.default_rng(K).choice(N, size=96, replace=False))
     check(got[:, cols], d, "gemm", f"gemm bf16 M={M} K={K} N={N} sampled", cols=cols)

@@ -1,8 +1,10 @@
 """Matmul calls captured in a HIP graph and replayed: every replay must equal
 the eager result bitwise (same kernels, same workspace, fixed summation
-orders).  The K-split kernels leave their arrival counters at zero after each
-call, which is what lets a captured call run again; eager work and
-synchronizations run between the replays."""
+orders).  The kernels that count arrivals (the decode GEMV and the streaming
+matrix-core form) leave their counters at zero after each call, and the tiled
+GEMMs park K-split partials that a second launch sums, which is what lets a
+captured call run again; eager work and synchronizations run between the
+replays."""
 from __future__ import annotations
 
 import numpy as np
