@@ -526,7 +526,7 @@ def main():
             "roofline": {"bound": "hbm", "achieved": round(gemv_gbs, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(gemv_gbs / PEAK_HBM_GBS, 4),
                          "traffic": recorded_traffic("tf_gemv.hip"),
-                         "kernel": "gemv_kernel<4,1,16,4,2,false>"},
+                         "kernel": "gemv_kernel<4,1,16,4,8,false> (one-round form)"},
         },
         "gemm_ms_per_step": round(gemm_ms, 4),
         "gemm_us_per_shape": {f"K={K},N={N}": round(t * 1e3, 2) for (M, K, N), t in zip(GEMM_SHAPES, shape_ms)},

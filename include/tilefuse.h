@@ -120,8 +120,11 @@ int tf_pack_w8_sym(const int8_t* qweight, const uint16_t* scales, int64_t K, int
 /*
  * Workspace the matmul entry points can use for this problem, in bytes (0
  * when the kernels chosen for it need none).  Negative tf_status on bad
- * arguments.  The workspace holds per-K-slice partial sums and arrival
- * counters; it lets the decode GEMV split K over many short workgroups.
+ * arguments.  The workspace holds per-K-slice partial sums (fp32) and, for
+ * the decode GEMV and the weight-streaming matrix-core form, arrival counters;
+ * it lets those kernels split K over more workgroups than there are output
+ * panels, and the tiled GEMMs split K (partials summed by a second launch in
+ * slice order) or share tiles between blocks (stream-K).
  *
  * Contract for every `workspace` argument below:
  *  - NULL selects kernels that need none (workspace_bytes is then ignored);

@@ -554,8 +554,9 @@ bool gemm256_supported(const Layout& L) {
 }
 
 // Stream-K is planned when the 256 x 256 tiles do not fill whole waves of
-// kSkMaxGroups blocks; its workspace is the arrival counters (at the shared
-// counter offset 0) and two partial tiles per block.
+// kSkMaxGroups blocks; its workspace is the shared counter region at offset 0
+// (the other kernels' arrival counters; this one leaves it untouched), then
+// two parked partial tiles per block.
 int64_t gemm256_workspace_bytes(const Layout& L, int64_t M) {
     const int64_t tiles = ((M + kBM - 1) / kBM) * ((L.N + kBN - 1) / kBN);
     if (!gemm256_supported(L) || tiles % kSkMaxGroups == 0) return 0;

@@ -84,7 +84,9 @@ struct WaveStage {
 
 // SEG > 0: segments (atoms summed before the scale is applied) have SEG
 // atoms, fixed at compile time (one group of 32 SEG rows); SEG = 0: group
-// size known at run time.  D: weight atoms a wave keeps in flight.
+// size known at run time.  D: weight atoms a wave keeps in flight; D = U is
+// the one-round form (the vector forms with at most U atoms per wave): every
+// atom of the run is requested at the start and nothing is refilled.
 template <int BITS, int M, int WAVES, int SEG, int D, bool BF>
 __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
@@ -100,14 +102,25 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     constexpr int MB = Cfg::MB;
     static_assert(SEG == 0 || U % SEG == 0, "segments tile a round");
     static_assert(U % D == 0, "the load ring tiles a round");
+    constexpr bool ONE = D == U && !MF;
     // metadata of the groups one round touches: U / SEG groups, or up to U
     constexpr int NGR = SEG > 0 ? U / SEG : U;
     constexpr int SLANES = NGR * PW * 2 / 16, ZLANES = NGR * PW / 8;
     using Stage = WaveStage<Cfg::XR, Cfg::CR, PW>;
-    union Smem {
+    // The vector forms keep the reduction buffer beside the staging areas
+    // (84 KB together at most, W4 with 3 rows; one workgroup per compute unit
+    // either way), so a wave that has finished writes its sums while others
+    // still read their staging, with no barrier in between; the matrix-core
+    // form's reduction buffer (up to 64 rows) reuses the staging storage.
+    struct SmemApart {
         Stage st[WAVES];
         float red[WAVES][M][PW];
     };
+    union SmemShared {
+        Stage st[WAVES];
+        float red[WAVES][M][PW];
+    };
+    using Smem = std::conditional_t<MF, SmemShared, SmemApart>;
     __shared__ __align__(16) Smem sm;
 
     const int p = blockIdx.x;
@@ -307,7 +320,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
             if (i > 0 && j >= nw) break;
             // take atom j from the ring and request atom j + D in its place
             const u32x4 wv = ring[i % D];
-            ring[i % D] = load_atom(j + D);
+            if constexpr (!ONE) ring[i % D] = load_atom(j + D);
             u32x4 afrag[MF ? MB : 1];
             if constexpr (MF) {
 #pragma unroll
@@ -434,18 +447,25 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 #pragma unroll
                 for (int b = 0; b < MB; ++b) aring[b][d] = load_afrag(b, d);
         }
-        // The next round's small loads are issued even past the last round,
-        // at clamped addresses: without a branch around a load the compiler's
-        // wait counts stay exact.  Round 0 is peeled off the loop for the same
-        // reason (waits after a loop header are conservative).
-        issue_meta(1, m1);
-        consume_round(0, m0);
-        for (int r = 1; r < nrounds; r += 2) {
-            issue_meta(r + 1, m0);
-            consume_round(r, m1);
-            if (r + 1 < nrounds) {
-                issue_meta(r + 2, m1);
-                consume_round(r + 1, m0);
+        if constexpr (ONE) {
+            // one round (the launcher's guarantee): no further requests, so
+            // the wave waits for no load it does not use before it ends
+            consume_round(0, m0);
+        } else {
+            // The next round's small loads are issued even past the last
+            // round, at clamped addresses: without a branch around a load the
+            // compiler's wait counts stay exact.  Round 0 is peeled off the
+            // loop for the same reason (waits after a loop header are
+            // conservative).
+            issue_meta(1, m1);
+            consume_round(0, m0);
+            for (int r = 1; r < nrounds; r += 2) {
+                issue_meta(r + 1, m0);
+                consume_round(r, m1);
+                if (r + 1 < nrounds) {
+                    issue_meta(r + 2, m1);
+                    consume_round(r + 1, m0);
+                }
             }
         }
     }
@@ -470,7 +490,6 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                 v += __shfl_xor(v, 32);
                 y[m][t] = v;
             }
-        __syncthreads();   // staging storage becomes the reduction buffer
         if (kg == 0) {
 #pragma unroll
             for (int m = 0; m < M; ++m)
@@ -549,6 +568,11 @@ constexpr int gemv_waves_for(int M) { return M <= 3 ? 16 : 8; }
 // Weight atoms in flight per wave.  Two measured best on MI355X (graph
 // replay, K=4096 N=14336 and K=14336 N=4096, M = 1..16): four or eight
 // lengthen the memory queues without raising the rate a compute unit streams.
+// A run of one round (at most kGemvU atoms per wave) is instead requested
+// whole at the start (the one-round form): no refill requests past its end and
+// no metadata for a round that does not come, each a round trip the wave
+// would wait for before it ends (measured: K=4096 with N=14336 W4 2%, N=32768
+// W4 10%, N=4096 W8 11% faster).
 constexpr int gemv_ring_for(int) { return 2; }
 
 inline GemvPlan plan_gemv(const Layout& L, int64_t M) {
@@ -588,9 +612,14 @@ int launch_g(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C,
     const int AS = split ? sp.AS : (int)L.na;
     int RW = (AS + WAVES - 1) / WAVES;               // atoms per wave
     if (SEG > 0) RW = (RW + SEG - 1) / SEG * SEG;    // runs start on group boundaries
-    return launch(gemv_kernel<BITS, M, WAVES, SEG, gemv_ring_for(M), BF>, dim3((unsigned)L.np, (unsigned)S),
-                  dim3(WAVES * 64), 0, s, A, pk, C, (int)L.K, (int)L.N, L.group, L.s_off, L.z_off,
-                  (int)L.na, (int)L.ng, S, AS, RW, part, cnt, mr);
+    auto go = [&](auto kernel) {
+        return launch(kernel, dim3((unsigned)L.np, (unsigned)S), dim3(WAVES * 64), 0, s, A, pk, C,
+                      (int)L.K, (int)L.N, L.group, L.s_off, L.z_off, (int)L.na, (int)L.ng, S, AS, RW,
+                      part, cnt, mr);
+    };
+    if constexpr (M <= TF_GEMV_MAX_M)
+        if (RW <= kGemvU) return go(gemv_kernel<BITS, M, WAVES, SEG, kGemvU, BF>);
+    return go(gemv_kernel<BITS, M, WAVES, SEG, gemv_ring_for(M), BF>);
 }
 
 template <int BITS, int M, bool BF>

@@ -154,6 +154,19 @@ def test_gemv_parity_small(tf, bits, M, K, N, G):
     assert_parity(run(tf, "gemv", d, pack(tf, d)), ref(d), f"gemv {bits} {M}x{K}x{N}")
 
 
+@pytest.mark.parametrize("bits,M,K,N,G", [(4, 1, 4096, 200, 128), (4, 1, 4224, 200, 128),
+                                           (8, 3, 4096, 104, 64), (8, 3, 4160, 104, 64),
+                                           (4, 2, 4096, 72, 32), (4, 2, 4128, 72, 32)])
+def test_gemv_one_round_boundary(tf, bits, M, K, N, G):
+    """With 16 waves, K = 4096 gives each wave a run of 8 atoms, requested
+    whole at the start (one round); one atom more per wave takes the
+    refilled ring of two rounds.  Both sides of that boundary, with segments
+    fixed at compile time (group 128) and known at run time."""
+    d = make_inputs(bits, M, K, N, group=G, seed=7 * K + N)
+    assert_parity(run(tf, "gemv", d, pack(tf, d), workspace=False), ref(d),
+                  f"gemv {bits} {M}x{K}x{N} G={G}")
+
+
 GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 200, 64),
                (8, 33, 256, 40, 128), (8, 130, 384, 104, 128), (4, 9, 96, 8, 32),
                (4, 300, 1024, 520, 128), (8, 64, 128, 4096, 128), (4, 1, 256, 64, 128),
