@@ -152,6 +152,35 @@ def test_workspace_query(lib):
     assert lib.tf_workspace_bytes(4, 16, 256, 64, 100) == tfb.TF_ERR_GROUP
 
 
+KIB = 1024
+COUNTERS = 8 * KIB          # arrival counters at offset 0: one u32 per 32 columns of TF_MAX_DIM
+
+
+@pytest.mark.parametrize("bits,M,K,N,want", [
+    # 256-row GEMM whose 256 x 256 tiles do not fill whole waves of 256
+    # blocks: two parked fp32 partial tiles per block
+    (4, 2048, 4096, 14336, COUNTERS + 2 * 256 * 256 * 256 * 4),
+    (4, 2048, 14336, 4096, COUNTERS + 2 * 256 * 256 * 256 * 4),
+    (4, 1024, 4096, 14336, COUNTERS + 2 * 256 * 256 * 256 * 4),
+    (4, 2048, 4096, 16384, 0),                       # 512 tiles: whole waves, no split
+    # 128-row GEMM split-K: one 128 x 256 fp32 partial per (tile, slice), and
+    # the slices bring the work to 256 units (64 tiles x 4, 32 tiles x 8)
+    (8, 512, 4096, 4096, COUNTERS + 256 * 128 * 256 * 4),
+    (8, 256, 4096, 4096, COUNTERS + 256 * 128 * 256 * 4),
+    # decode GEMV on 64 panels of 64 columns, K split in 4 slices: one fp32
+    # partial per (panel, slice, row)
+    (4, 1, 14336, 4096, COUNTERS + 64 * 4 * 1 * 64 * 4),
+    (4, 3, 14336, 4096, COUNTERS + 64 * 4 * 3 * 64 * 4),
+    # GEMM entry with 40 rows: the streaming matrix-core form, 64 row slots
+    (4, 40, 14336, 4096, COUNTERS + 64 * 4 * 64 * 64 * 4),
+    (4, 1, 4096, 14336, 0),                          # 224 panels fill the chip: no split
+])
+def test_workspace_sizes(lib, bits, M, K, N, want):
+    """The workspace each documented plan asks for: the counter region, then
+    the fp32 partials its K split parks."""
+    assert lib.tf_workspace_bytes(bits, M, K, N, 128) == want
+
+
 @pytest.mark.parametrize("bits", [4, 8])
 def test_workspace_rejects(lib, bits):
     need = lib.tf_workspace_bytes(bits, 1, 14336, 2048, 128)
