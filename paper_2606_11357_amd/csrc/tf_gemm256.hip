@@ -593,10 +593,15 @@ int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16
     // split ("hybrid"): fewer partial tiles than splitting everything, no
     // idle units in the last wave.
     // Whole tiles while they keep at least 80% of the launch's block slots
-    // busy (ceil(tiles / cus) waves of cus blocks); measured on MI355X over
-    // the M = 256..8192 sweep, the hybrid below loses to whole tiles there.
+    // busy (ceil(tiles / cus) waves of cus blocks) and their last wave holds
+    // at least 40% of the blocks.  Measured on MI355X (hybrid against whole
+    // tiles): K=4096, N=14336 at M = 4864, 5888, 7168 (last wave 16%, 3%,
+    // 12.5% full) 5-6% faster; at M = 2816 (41%) 1.4%, at M = 2048 (75%) 11%
+    // slower; K=14336, N=4096 at M = 6656 (62.5%) 4% faster; stream-K over
+    // fewer tiles than blocks (M = 3328, 81%) 11% slower.
     const int64_t waves = (tiles + cus - 1) / cus;
-    const bool dp_ok = 5 * (int64_t)tiles >= 4 * waves * cus;
+    const int64_t last = tiles - (waves - 1) * cus;        // tiles in the last wave
+    const bool dp_ok = 5 * (int64_t)tiles >= 4 * waves * cus && 5 * last >= 2 * cus;
     if (ws && need > 0 && (int64_t)ws_bytes >= need && !dp_ok) {
         int G = std::min(cus, kSkMaxGroups);
         if (G > kXcds) G -= G % kXcds;

@@ -362,6 +362,17 @@ def test_gemm_w4_large_sampled(tf, M, K, N, xstd):
 
 
 @pytest.mark.slow
+def test_gemm_hybrid_one_chunk_per_block(tf):
+    """264 tiles of 256 x 256 (M=2048, N=8448) at K=4096, 32 K chunks per tile,
+    on 256 blocks: one whole wave of tiles, then the last 8 tiles split over
+    all blocks, one K chunk each (32 segments per tile, summed by the
+    reduction launch), the smallest remainder the hybrid schedule takes.  All
+    of C against the oracle."""
+    d = make_inputs(4, 2048, 4096, 8448, seed=5)
+    assert_parity(run(tf, "gemm", d, pack(tf, d)), ref(d), "W4 GEMM hybrid, one K chunk per block")
+
+
+@pytest.mark.slow
 @pytest.mark.parametrize("M", [256, 1280, 4352, 8192])
 @pytest.mark.parametrize("K,N", [(4096, 14336), (14336, 4096)])
 def test_gemm_w4_msweep_sampled(tf, M, K, N):
