@@ -246,6 +246,14 @@ def test_gemm_bf16_full_size_sampled(tf, M, K, N, xstd):
     check(got[:, cols], d, "gemm", f"gemm bf16 M={M} K={K} N={N} sampled", cols=cols)
 
 
+def test_gemm_bf16_hybrid_one_chunk_per_block(tf):
+    """264 tiles of 256 x 256 (M=2048, N=8448) at K=4096 on 256 blocks: one
+    whole wave, then the last 8 tiles split over all blocks one K chunk each,
+    summed by the reduction launch in its BF16 form.  All of C."""
+    d = make_inputs_bf16(4, 2048, 4096, 8448, group=128, seed=11)
+    check(run(tf, "gemm", d, pack(tf, d)), d, "gemm", "gemm bf16 hybrid, one K chunk per block")
+
+
 def test_gemv_bf16_full_size(tf):
     """The decode GEMV at K = 4096, N = 14336 (M = 1), every output."""
     d = make_inputs_bf16(4, 1, 4096, 14336, group=128, seed=3)
