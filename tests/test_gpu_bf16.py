@@ -200,7 +200,7 @@ GEMV_CASES = [(4, 4096, 1032, 128), (8, 4096, 1032, 128), (4, 14336, 512, 128),
               (8, 14336, 512, 128), (4, 1024, 264, 64), (8, 2048, 136, 32), (4, 480, 264, 96)]
 
 
-@pytest.mark.parametrize("M", [1, 2, 3, 4, 5, 8])
+@pytest.mark.parametrize("M", [1, 2, 3, 4, 5, 6, 7, 8])
 @pytest.mark.parametrize("bits,K,N,G", GEMV_CASES)
 def test_gemv_bf16(tf, bits, M, K, N, G):
     d = make_inputs_bf16(bits, M, K, N, group=G, seed=M + K + N + G)
@@ -233,17 +233,33 @@ def test_integer_invariant_bf16(tf, bits, kind, M, K, N):
     assert_bf16_equal(got, oracle.bf16_encode(oracle.to_bf16(exact)))
 
 
+def check_blocked(got, d, kind, what, block=2048):
+    """``check`` over all of C, the oracle computed one block of output
+    columns at a time (bounded host memory at the 32K-dimension shapes); the
+    stated tolerance is applied to the whole matrix, the per-element bound to
+    every element."""
+    N = d["N"]
+    want = np.empty(got.shape, dtype=np.float64)
+    path = np.empty(got.shape, dtype=np.float64) if factored(kind, d["x_bits"].shape[0]) else want
+    for c0 in range(0, N, block):
+        cols = np.arange(c0, min(N, c0 + block))
+        want[:, cols] = ref(d, cols=cols)
+        if path is not want:
+            path[:, cols] = ref(d, cols=cols, exact=True)
+    return assert_parity(got, want, what, path)
+
+
+@pytest.mark.slow
 @pytest.mark.parametrize("M,K,N,xstd", [(2048, 4096, 14336, 1.0), (2048, 14336, 4096, 1.0),
                                          (1024, 4096, 32768, 0.5), (1024, 32768, 8192, 0.5)])
-def test_gemm_bf16_full_size_sampled(tf, M, K, N, xstd):
-    """The Llama-3-8B MLP shapes at M = 2048 in the benchmark's launch
-    configuration (default workspace) and the 32K-dimension shapes at
-    M = 1024: 96 sampled output columns, all rows."""
+def test_gemm_bf16_full_size(tf, M, K, N, xstd):
+    """The Llama-3-8B MLP shapes at M = 2048 and the 32K-dimension shapes at
+    M = 1024, in the benchmark's launch configuration (default workspace):
+    every element of C."""
     G = 128
     d = make_inputs_bf16(4, M, K, N, group=G, seed=K + 2 * N, x_std=xstd)
     got = run(tf, "gemm", d, pack(tf, d))
-    cols = np.sort(np.random.default_rng(K).choice(N, size=96, replace=False))
-    check(got[:, cols], d, "gemm", f"gemm bf16 M={M} K={K} N={N} sampled", cols=cols)
+    check_blocked(got, d, "gemm", f"gemm bf16 M={M} K={K} N={N} full")
 
 
 def test_gemm_bf16_hybrid_one_chunk_per_block(tf):

@@ -64,17 +64,15 @@ def test_mlp_composite_parity(tf, M, K, I):
 
 
 @pytest.mark.slow
-def test_mlp_llama3_8b_sampled(tf):
-    """Llama-3-8B MLP (hidden 4096, intermediate 14336) at M = 256: sampled rows
-    of Y against the oracle composite of those rows."""
+def test_mlp_llama3_8b_full(tf):
+    """Llama-3-8B MLP (hidden 4096, intermediate 14336) at M = 256: every
+    element of Y against the oracle composite."""
     M, K, I = 256, 4096, 14336
     gu, dn = _mlp_inputs(M, K, I, seed=3)
     got = _run_mlp(tf, gu, dn, K, I)
-    assert np.all(np.isfinite(got.astype(np.float64)))
-    rows = np.array([0, 17, 100, 255])
-    want = oracle.mlp_w4a16(gu["x"][rows], gu["qweight"], gu["qzeros"], gu["s"],
+    want = oracle.mlp_w4a16(gu["x"], gu["qweight"], gu["qzeros"], gu["s"],
                             dn["qweight"], dn["qzeros"], dn["s"], 128)
-    assert_parity(got[rows], want, "Llama-3-8B MLP sampled rows")
+    assert_parity(got, want, "Llama-3-8B MLP, all of Y")
 
 
 # ---------------------------------------------------------------------------
