@@ -24,11 +24,16 @@
  *  - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *    Calls only enqueue work on `stream` and return; the caller synchronizes.
  *  - The caller allocates and frees every buffer; the library keeps no device
- *    memory and no mutable global state, so calls are thread-safe.
+ *    memory.  Its only global state is a per-device cache of the compute-unit
+ *    count (read atomically; the launch plans depend on it), so calls are
+ *    thread-safe.  Plans are made for the device of the `stream` argument.
  *  - Arguments are validated before any HIP call; a rejected call enqueues
  *    nothing.  Only TF_ERR_HIP comes from the runtime (launch failure).
  *  - Outputs must not overlap inputs.
- *  - No C++ exception crosses this boundary; the library prints nothing.
+ *  - No C++ exception crosses this boundary.  The library prints nothing,
+ *    except with the environment variable TF_LOG=1 (read once, at the first
+ *    matmul call): each matmul call then writes one line to stderr naming the
+ *    kernel it launched and its plan (tiles, K slices, stream-K blocks).
  */
 #ifndef TILEFUSE_H
 #define TILEFUSE_H
@@ -135,6 +140,15 @@ int tf_pack_w8_sym(const int8_t* qweight, const uint16_t* scales, int64_t K, int
  *  - calls that may run concurrently must not share one workspace.
  */
 int64_t tf_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group);
+
+/*
+ * The same query under the name of the GEMM's workspace (the prefill GEMM
+ * is the main user of a workspace: stream-K or split-K partial tiles).  It
+ * returns exactly tf_workspace_bytes(bits, M, K, N, group), which already
+ * covers every kernel the GEMM and GEMV entry points can choose for M rows,
+ * so one buffer of that size serves either call.
+ */
+int64_t tf_gemm_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group);
 
 /*
  * Prefill GEMM (Section 2.1: M grows with the prompt length):

@@ -46,32 +46,58 @@ EXTRA = {
 }
 
 
-def _compile(src: str, obj: str) -> None:
-    cmd = [HIPCC, *FLAGS, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
+def _compile(src: str, obj: str, extra=()) -> None:
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(os.path.basename(src), []), *extra, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {os.path.basename(src)}:\n{r.stderr}")
 
 
-def build(verbose: bool = False) -> str:
+def _sources():
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     if not srcs:
         raise RuntimeError("no HIP sources found")
+    return srcs
+
+
+def _build_into(out: str, compile_extra=(), link_extra=()) -> str:
+    srcs = _sources()
     tmp = tempfile.mkdtemp(prefix="tf_build_")
     try:
         objs = [os.path.join(tmp, os.path.basename(s) + ".o") for s in srcs]
         with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-            list(ex.map(_compile, srcs, objs))
-        out_tmp = LIB + ".tmp"
-        cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", out_tmp, *objs]
+            list(ex.map(lambda so: _compile(so[0], so[1], compile_extra), zip(srcs, objs)))
+        out_tmp = out + ".tmp"
+        cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *link_extra, "-o", out_tmp, *objs]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"link failed:\n{r.stderr}")
-        os.replace(out_tmp, LIB)
+        os.replace(out_tmp, out)
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
+    return out
+
+
+PROBE_SRC = os.path.join(PKG, "probe", "read_probe.hip")
+PROBE_LIB = os.path.join(PKG, "probe", "libtf_read_probe.so")
+
+
+def build_probe() -> str:
+    """The streaming-read probe the benchmark's context figures use (a
+    library of its own, not part of libtilefuse)."""
+    cmd = [HIPCC, *FLAGS, "-shared", PROBE_SRC, "-o", PROBE_LIB + ".tmp"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for read_probe.hip:\n{r.stderr}")
+    os.replace(PROBE_LIB + ".tmp", PROBE_LIB)
+    return PROBE_LIB
+
+
+def build(verbose: bool = False) -> str:
+    _build_into(LIB)
+    build_probe()
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {PROBE_LIB}")
     return LIB
 
 

@@ -1,6 +1,51 @@
 // C-ABI entry points of libtilefuse: argument validation (always before any
-// HIP call), layout sizing, and dispatch to the kernel launchers.
+// HIP call), layout sizing, and dispatch to the kernel launchers; and the
+// host services the launchers share (device properties, plan logging).
+#include <atomic>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+
 #include "tf_internal.h"
+
+namespace tf {
+
+int device_cus(hipStream_t stream) {
+    constexpr int kMaxDevices = 64;
+    constexpr int kFallback = 256;          // MI355X: 256 compute units
+    // one slot per device; every writer stores the same value, read and
+    // written atomically
+    static std::atomic<int> cus[kMaxDevices];
+    int dev = -1;
+    if (hipStreamGetDevice(stream, &dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return kFallback;
+    int n = cus[dev].load(std::memory_order_relaxed);
+    if (n > 0) return n;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+        return kFallback;
+    cus[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
+
+bool log_enabled() {
+    static const bool on = [] {
+        const char* e = std::getenv("TF_LOG");
+        return e != nullptr && e[0] == '1' && e[1] == '\0';
+    }();
+    return on;
+}
+
+void log_plan(const char* fmt, ...) {
+    if (!log_enabled()) return;
+    char line[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(line, sizeof line, fmt, ap);
+    va_end(ap);
+    std::fprintf(stderr, "[tilefuse] %s\n", line);
+}
+
+}  // namespace tf
 
 namespace {
 
@@ -139,6 +184,10 @@ int64_t tf_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group)
     if (rc) return rc;
     if (M < 1 || M > TF_MAX_M) return TF_ERR_SHAPE;
     return workspace_bytes(tf::make_layout(bits, K, N, group), M);
+}
+
+int64_t tf_gemm_workspace_bytes(int bits, int64_t M, int64_t K, int64_t N, int group) {
+    return tf_workspace_bytes(bits, M, K, N, group);
 }
 
 int tf_w4a16_gemm(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,

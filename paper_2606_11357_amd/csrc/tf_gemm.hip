@@ -468,6 +468,10 @@ int launch_main(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t*
     if (!ws) sp = {1, (int)(L.K / (kBK * chunk_steps<BITS>()))};
     SplitK sk{sp.S, sp.cps, nullptr};
     if (sp.S > 1) sk.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes);
+    if (log_enabled())
+        log_plan("gemm_kernel<%d,%d,%s> M=%lld K=%lld N=%lld G=%d: %dx%d tiles of 128x256, %d K slices of "
+                 "%d chunks%s", BITS, MPC, BF ? "bf16" : "f16", (long long)M, (long long)L.K, (long long)L.N,
+                 L.group, tiles_m, tiles_n, sp.S, sp.cps, sp.S > 1 ? ", reduction launch" : "");
     const int rc = launch(gemm_kernel<BITS, MPC, BF>, dim3((unsigned)(tiles_m * tiles_n * sp.S)),
                           dim3(kGemmThreads), 0, s, A, pk, C, (int)M, (int)L.K, (int)L.N, gshift, L.s_off,
                           L.z_off, (int)L.na, (int)L.ng, (int)L.np, tiles_m, tiles_n, sk);
@@ -490,6 +494,9 @@ int launch_bits(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t*
         if constexpr (CS >= 4) return launch_main<BITS, 4, BF>(L, A, pk, C, M, ws, s);
     }
     dim3 grid((unsigned)((L.N + kBN1 - 1) / kBN1), (unsigned)((M + kBM1 - 1) / kBM1));
+    if (log_enabled())
+        log_plan("gemm_kernel_generic<%d,%s> M=%lld K=%lld N=%lld G=%d: %ux%u tiles of 128x128", BITS,
+                 BF ? "bf16" : "f16", (long long)M, (long long)L.K, (long long)L.N, L.group, grid.y, grid.x);
     return launch(gemm_kernel_generic<BITS, BF>, grid, dim3(kGemmThreads), 0, s, A, pk, C, (int)M,
                   (int)L.K, (int)L.N, L.group, L.s_off, L.z_off, (int)L.na, (int)L.ng, (int)L.np);
 }
@@ -500,8 +507,8 @@ int launch_bits(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t*
 // device or a workspace lets it split K (it is then the only GEMM that uses
 // a workspace); below that its 256-row tiles leave too little parallelism.
 constexpr int64_t kGemm256MinM = 1024;
-static bool use_gemm256(const Layout& L, int64_t M, const void* ws) {
-    return M >= kGemm256MinM && gemm256_supported(L) && (ws != nullptr || gemm256_fills_device(L, M));
+static bool use_gemm256(const Layout& L, int64_t M, const void* ws, hipStream_t s) {
+    return M >= kGemm256MinM && gemm256_supported(L) && (ws != nullptr || gemm256_fills_device(L, M, s));
 }
 
 // Workspace either GEMM may use for this problem: the 256-row kernel's
@@ -516,7 +523,7 @@ int64_t gemm_workspace_bytes(const Layout& L, int64_t M) {
 int launch_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, size_t ws_bytes, hipStream_t s, bool bf) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    if (use_gemm256(L, M, ws)) return launch_gemm256(L, A, pk, C, M, ws, ws_bytes, s, bf);
+    if (use_gemm256(L, M, ws, s)) return launch_gemm256(L, A, pk, C, M, ws, ws_bytes, s, bf);
     // a workspace too small for this kernel's split (sized for another
     // kernel of a larger M) selects the single-pass form
     if (ws && (int64_t)ws_bytes < gemm_workspace_bytes(L, M)) ws = nullptr;

@@ -530,21 +530,6 @@ int launch_mpc(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* 
                   tiles_m, tiles_n, col_major, sk);
 }
 
-// Compute units of the current device (cached per device; the value never
-// changes, so a race between first callers only stores the same number).
-int device_cus() {
-    static int cus[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return kSkMaxGroups;
-    if (cus[dev] == 0) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-            return kSkMaxGroups;
-        cus[dev] = n;
-    }
-    return cus[dev];
-}
-
 }  // namespace
 
 bool gemm256_supported(const Layout& L) {
@@ -585,7 +570,7 @@ int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16
     const int tiles_n = (int)((L.N + kBN - 1) / kBN);
     const int tiles = tiles_m * tiles_n, chunks = (int)(L.K / (kBK * kCS));
     const int64_t need = gemm256_workspace_bytes(L, M);
-    const int cus = device_cus();
+    const int cus = device_cus(s);
     StreamK sk{0, 0, nullptr, 0};
     // Otherwise (with a workspace) stream-K; splitting every tile keeps at
     // least kSkMinUnits K chunks per block.  With at least one full wave of
@@ -619,6 +604,17 @@ int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16
         sk = StreamK{G, (int)units, reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsCounterBytes),
                      dp_rounds};
     }
+    if (log_enabled())
+        log_plan("gemm256_kernel<%d,%d,%s> M=%lld K=%lld N=%lld G=%d: %dx%d tiles of 256x256, %d K chunks, "
+                 "%s, %d CUs, order %s",
+                 L.bits, L.group >= kBK * kCS ? 1 : kBK * kCS / L.group, bf ? "bf16" : "f16", (long long)M,
+                 (long long)L.K, (long long)L.N, L.group, tiles_m, tiles_n, chunks,
+                 sk.groups == 0 ? "whole tiles"
+                 : sk.dp_rounds > 0 ? "hybrid (whole-tile rounds, then stream-K)" : "stream-K",
+                 cus, col_major_for(L, M) ? "column-major" : "row-major");
+    if (log_enabled() && sk.groups)
+        log_plan("  stream-K: %d blocks, %d whole-tile rounds, %d units, reduction launch over %d tiles",
+                 sk.groups, sk.dp_rounds, sk.units, tiles - sk.dp_rounds * sk.groups);
     const int rc = bf ? launch_bf<true>(L, A, pk, C, M, sk, tiles_m, tiles_n, s)
                       : launch_bf<false>(L, A, pk, C, M, sk, tiles_m, tiles_n, s);
     if (rc || sk.groups == 0) return rc;
@@ -634,9 +630,9 @@ int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16
                   tiles_n, cm, sk.groups, sk.units, chunks, tile0, total);
 }
 
-bool gemm256_fills_device(const Layout& L, int64_t M) {
+bool gemm256_fills_device(const Layout& L, int64_t M, hipStream_t s) {
     const int64_t tiles = ((M + kBM - 1) / kBM) * ((L.N + kBN - 1) / kBN);
-    return 4 * tiles >= 3 * (int64_t)device_cus();
+    return 4 * tiles >= 3 * (int64_t)device_cus(s);
 }
 
 }  // namespace tf

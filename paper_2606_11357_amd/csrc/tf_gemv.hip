@@ -612,14 +612,20 @@ int launch_g(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C,
     const int AS = split ? sp.AS : (int)L.na;
     int RW = (AS + WAVES - 1) / WAVES;               // atoms per wave
     if (SEG > 0) RW = (RW + SEG - 1) / SEG * SEG;    // runs start on group boundaries
-    auto go = [&](auto kernel) {
+    auto go = [&](auto kernel, int d) {
+        if (log_enabled())
+            log_plan("gemv_kernel<%d,%d,%d,%d,%d,%s> rows=%d K=%lld N=%lld G=%d: %s form, %lld panels x %d K "
+                     "slices of %d atoms, %d atoms per wave%s", BITS, M, WAVES, SEG, d, BF ? "bf16" : "f16", mr,
+                     (long long)L.K, (long long)L.N, L.group,
+                     M > TF_GEMV_MAX_M ? "matrix-core" : (d == kGemvU ? "one-round vector" : "vector"),
+                     (long long)L.np, S, AS, RW, split ? ", partials summed by the last slice" : "");
         return launch(kernel, dim3((unsigned)L.np, (unsigned)S), dim3(WAVES * 64), 0, s, A, pk, C,
                       (int)L.K, (int)L.N, L.group, L.s_off, L.z_off, (int)L.na, (int)L.ng, S, AS, RW,
                       part, cnt, mr);
     };
     if constexpr (M <= TF_GEMV_MAX_M)
-        if (RW <= kGemvU) return go(gemv_kernel<BITS, M, WAVES, SEG, kGemvU, BF>);
-    return go(gemv_kernel<BITS, M, WAVES, SEG, gemv_ring_for(M), BF>);
+        if (RW <= kGemvU) return go(gemv_kernel<BITS, M, WAVES, SEG, kGemvU, BF>, kGemvU);
+    return go(gemv_kernel<BITS, M, WAVES, SEG, gemv_ring_for(M), BF>, gemv_ring_for(M));
 }
 
 template <int BITS, int M, bool BF>

@@ -487,6 +487,18 @@ __device__ __forceinline__ u32x4 dq_operand(uint32_t w0, uint32_t w1, uint32_t m
 
 }  // namespace tf
 
+// Host services shared by the launchers (tf_api.hip).
+namespace tf {
+// Compute units of the device that `stream` belongs to (NULL: the current
+// device), queried once per device and cached; 256 if the runtime cannot
+// tell.  Safe to call from several threads at once.
+int device_cus(hipStream_t stream);
+// Whether TF_LOG=1 is set (read once); log_plan() then writes one line per
+// matmul call to stderr naming the kernel and launch plan it chose.
+bool log_enabled();
+void log_plan(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
+}  // namespace tf
+
 // Launchers implemented in the kernel sources (called by tf_api.hip after
 // argument validation).
 namespace tf {
@@ -508,7 +520,7 @@ int launch_skinny_gemm(const Layout& L, const uint16_t* A, const void* packed, u
                        int64_t M, void* ws, hipStream_t s, bool bf);
 int64_t gemm_workspace_bytes(const Layout& L, int64_t M);
 bool gemm256_supported(const Layout& L);
-bool gemm256_fills_device(const Layout& L, int64_t M);
+bool gemm256_fills_device(const Layout& L, int64_t M, hipStream_t s);
 int64_t gemm256_workspace_bytes(const Layout& L, int64_t M);
 int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
                    void* ws, size_t ws_bytes, hipStream_t s, bool bf);

@@ -11,7 +11,9 @@ import ctypes
 import os
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libtilefuse.so")
+# TILEFUSE_LIB names another build of the same library to load instead (the
+# host-sanitizer build the CPU tests run the argument checks under).
+LIB_PATH = os.environ.get("TILEFUSE_LIB") or os.path.join(PKG, "libtilefuse.so")
 
 TF_OK = 0
 TF_ERR_NULL = -1
@@ -27,8 +29,8 @@ GEMV_MAX_M = 8
 
 EXPORTS = (
     "tf_layout_version", "tf_status_str", "tf_packed_bytes", "tf_pack_w4", "tf_pack_w8",
-    "tf_pack_w8_sym", "tf_workspace_bytes", "tf_w4a16_gemm", "tf_w8a16_gemm", "tf_w4a16_gemv",
-    "tf_w8a16_gemv", "tf_w4a16_gemm_bf16", "tf_w8a16_gemm_bf16", "tf_w4a16_gemv_bf16",
+    "tf_pack_w8_sym", "tf_workspace_bytes", "tf_gemm_workspace_bytes", "tf_w4a16_gemm",
+    "tf_w8a16_gemm", "tf_w4a16_gemv", "tf_w8a16_gemv", "tf_w4a16_gemm_bf16", "tf_w8a16_gemm_bf16", "tf_w4a16_gemv_bf16",
     "tf_w8a16_gemv_bf16", "tf_unpack", "tf_dequant", "tf_silu_mul", "tf_silu_mul_bf16",
 )
 
@@ -60,6 +62,7 @@ def load() -> ctypes.CDLL:
         "tf_pack_w8": (I, [P, P, P, I64, I64, I, P, P]),
         "tf_pack_w8_sym": (I, [P, P, I64, I64, I, P, P]),
         "tf_workspace_bytes": (I64, [I, I64, I64, I64, I]),
+        "tf_gemm_workspace_bytes": (I64, [I, I64, I64, I64, I]),
         "tf_w4a16_gemm": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_w8a16_gemm": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_w4a16_gemv": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),

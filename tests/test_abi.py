@@ -247,3 +247,12 @@ def test_binding_refuses_cpu_tensors():
 def test_silu_mul_rejects(lib, args, want):
     assert lib.tf_silu_mul(*args) == want
     assert lib.tf_silu_mul_bf16(*args) == want
+
+
+@pytest.mark.parametrize("args", [(4, 2048, 4096, 14336, 128), (8, 512, 4096, 4096, 128), (4, 1, 14336, 4096, 128),
+                                  (4, 40, 14336, 4096, 128), (8, 3, 4096, 4096, 64), (4, 0, 256, 64, 128),
+                                  (4, 16, 256, 64, 100), (5, 16, 256, 64, 128)])
+def test_gemm_workspace_query_is_the_workspace_query(lib, args):
+    """tf_gemm_workspace_bytes answers exactly what tf_workspace_bytes does,
+    sizes and errors alike."""
+    assert lib.tf_gemm_workspace_bytes(*args) == lib.tf_workspace_bytes(*args)
