@@ -186,6 +186,25 @@ int tf_w8a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,
                   void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * tf_w4a16_gemv without a workspace argument and without any allocation, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops that forbid hipMalloc).  Same operands, checks, kernels and
+ * result as tf_w4a16_gemv with a workspace: where the decode GEMV splits K,
+ * its partial sums and arrival counters live in a scratch array of 1 MiB in
+ * the library's static device memory, one per GPU, held until the process
+ * ends (every shape the GEMV entry points accept needs at most about 0.9 MiB;
+ * a larger need returns TF_ERR_ARG).  The call allocates nothing: the first
+ * call on a device looks up that device's copy of the array and enqueues one
+ * small kernel on `stream` that zeroes its counters (again at the next call
+ * outside stream capture if the first was captured); every call leaves the
+ * counters at zero.  All calls on one GPU share its array, so calls that may
+ * run concurrently on one GPU (different streams, not ordered by events)
+ * race and must not overlap.
+ */
+int tf_w4a16_gemv_noalloc(const uint16_t* A_f16, const void* packed, uint16_t* C_f16,
+                          int64_t M, int64_t K, int64_t N, int group, void* stream);
+
+/*
  * BF16 activations and scales (the paper's dtype: Section 2.2 takes BF16
  * activations, Section 4.2 stores BF16 scales beside each weight tile,
  * Section 4.3 holds the dequantized weights in BF16 before the multiply):

@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <mutex>
 
 #include "tf_internal.h"
 
@@ -115,11 +116,71 @@ int gemv_entry(int bits, const uint16_t* A, const void* packed, uint16_t* C, int
     return tf::launch_gemv(L, A, packed, C, M, ws, static_cast<hipStream_t>(stream), bf);
 }
 
+// ---- Scratch of the allocation-free decode GEMV (tf_w4a16_gemv_noalloc):
+// one array of kScratchBytes per device in the library's static device
+// memory, held until the process ends.  Host code never passes the array's
+// name to a kernel (in host code it is a host-side stand-in): it asks the
+// runtime once per device for the array's device address and uses that.
+constexpr int64_t kScratchBytes = int64_t(1) << 20;
+constexpr int kScratchDevices = 64;
+
+__global__ void clear_words_kernel(uint32_t* p, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0u;
+}
+
+struct ScratchSlot {
+    void* ptr;        // device address of `scratch` on this device, once known
+    bool cleared;     // counters cleared by a launch outside stream capture
+};
+std::mutex g_scratch_mu;
+ScratchSlot g_scratch[kScratchDevices];
+
 int silu_mul_entry(const uint16_t* GU, int64_t M, int64_t N, uint16_t* H, void* stream, bool bf) {
     if (!GU || !H) return TF_ERR_NULL;
     if (M < 1 || M > TF_MAX_M || N <= 0 || N > TF_MAX_DIM || N % 8 != 0) return TF_ERR_SHAPE;
     if (misaligned(GU) || misaligned(H)) return TF_ERR_ALIGN;
     return tf::launch_silu_mul(GU, M, N, H, static_cast<hipStream_t>(stream), bf);
+}
+
+}  // namespace
+
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+
+// The scratch of the device `s` belongs to.  The first call on a device looks
+// up its address (with that device current) and enqueues a clear of the
+// arrival counters on `s`; every GEMV leaves the counters it used at zero, so
+// later calls need no clear.  A clear recorded into a graph under capture
+// does not count as done (the graph may never be launched): the next call
+// outside capture clears again.
+int scratch_for(hipStream_t s, void** out) {
+    int dev = -1;
+    if (hipStreamGetDevice(s, &dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return TF_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    ScratchSlot& slot = g_scratch[dev];
+    if (slot.ptr == nullptr) {
+        int cur = -1;
+        if (hipGetDevice(&cur) != hipSuccess) return TF_ERR_HIP;
+        if (cur != dev && hipSetDevice(dev) != hipSuccess) return TF_ERR_HIP;
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur != dev && hipSetDevice(cur) != hipSuccess) return TF_ERR_HIP;
+        if (e != hipSuccess || p == nullptr) return TF_ERR_HIP;
+        slot.ptr = p;
+    }
+    if (!slot.cleared) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(s, &cs) != hipSuccess) return TF_ERR_HIP;
+        constexpr int kWords = (int)(tf::kWsCounterBytes / 4);
+        const int rc = tf::launch(clear_words_kernel, dim3((kWords + 255) / 256), dim3(256), 0, s,
+                                  static_cast<uint32_t*>(slot.ptr), kWords);
+        if (rc) return rc;
+        if (cs == hipStreamCaptureStatusNone) slot.cleared = true;
+    }
+    *out = slot.ptr;
+    return TF_OK;
 }
 
 }  // namespace
@@ -230,6 +291,20 @@ int tf_w4a16_gemv_bf16(const uint16_t* A_bf16, const void* packed, uint16_t* C_b
                        void* stream) {
     return gemv_entry(4, A_bf16, packed, C_bf16, M, K, N, group, workspace, workspace_bytes, stream,
                       true);
+}
+
+int tf_w4a16_gemv_noalloc(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,
+                          int64_t K, int64_t N, int group, void* stream) {
+    int rc = check_matmul(4, A_f16, packed, C_f16, M, K, N, group);
+    if (rc) return rc;
+    if (M > TF_GEMV_MAX_M) return TF_ERR_ARG;
+    const Layout L = tf::make_layout(4, K, N, group);
+    if (tf::gemv_workspace_bytes(L, M) > kScratchBytes) return TF_ERR_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void* ws = nullptr;
+    rc = scratch_for(s, &ws);
+    if (rc) return rc;
+    return tf::launch_gemv(L, A_f16, packed, C_f16, M, ws, s, false);
 }
 
 int tf_w8a16_gemv(const uint16_t* A_f16, const void* packed, uint16_t* C_f16, int64_t M,

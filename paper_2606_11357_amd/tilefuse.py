@@ -30,7 +30,7 @@ GEMV_MAX_M = 8
 EXPORTS = (
     "tf_layout_version", "tf_status_str", "tf_packed_bytes", "tf_pack_w4", "tf_pack_w8",
     "tf_pack_w8_sym", "tf_workspace_bytes", "tf_gemm_workspace_bytes", "tf_w4a16_gemm",
-    "tf_w8a16_gemm", "tf_w4a16_gemv", "tf_w8a16_gemv", "tf_w4a16_gemm_bf16", "tf_w8a16_gemm_bf16", "tf_w4a16_gemv_bf16",
+    "tf_w8a16_gemm", "tf_w4a16_gemv", "tf_w8a16_gemv", "tf_w4a16_gemv_noalloc", "tf_w4a16_gemm_bf16", "tf_w8a16_gemm_bf16", "tf_w4a16_gemv_bf16",
     "tf_w8a16_gemv_bf16", "tf_unpack", "tf_dequant", "tf_silu_mul", "tf_silu_mul_bf16",
 )
 
@@ -67,6 +67,7 @@ def load() -> ctypes.CDLL:
         "tf_w8a16_gemm": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_w4a16_gemv": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_w8a16_gemv": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
+        "tf_w4a16_gemv_noalloc": (I, [P, P, P, I64, I64, I64, I, P]),
         "tf_w4a16_gemm_bf16": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_w8a16_gemm_bf16": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
         "tf_w4a16_gemv_bf16": (I, [P, P, P, I64, I64, I64, I, P, SZ, P]),
@@ -230,6 +231,23 @@ def w4a16_gemv(A, packed, K: int, N: int, group: int = 128, out=None, workspace=
 
 def w8a16_gemv(A, packed, K: int, N: int, group: int = 128, out=None, workspace=None):
     return _matmul(8, "gemv", A, packed, K, N, group, out, workspace)
+
+
+def w4a16_gemv_noalloc(A, packed, K: int, N: int, group: int = 128, out=None):
+    """The decode GEMV through tf_w4a16_gemv_noalloc: no workspace argument, the
+    library's static per-device scratch instead (A fp16 [M, K], 1 <= M <= 8)."""
+    torch = _torch()
+    _need_cuda(A, packed, out)
+    M = A.shape[0]
+    if A.dtype != torch.float16 or A.dim() != 2 or A.shape[1] != K:
+        raise ValueError("A must be fp16 [M, K]")
+    if out is None:
+        out = torch.empty((M, N), dtype=A.dtype, device=A.device)
+    elif out.dtype != A.dtype or tuple(out.shape) != (M, N):
+        raise ValueError("out must have A's dtype and shape [M, N]")
+    _check(load().tf_w4a16_gemv_noalloc(_ptr(A), _ptr(packed), _ptr(out), M, K, N, group, _stream(A.device)),
+           "tf_w4a16_gemv_noalloc")
+    return out
 
 
 def unpack(bits: int, packed, K: int, N: int, group: int = 128):

@@ -256,3 +256,11 @@ def test_gemm_workspace_query_is_the_workspace_query(lib, args):
     """tf_gemm_workspace_bytes answers exactly what tf_workspace_bytes does,
     sizes and errors alike."""
     assert lib.tf_gemm_workspace_bytes(*args) == lib.tf_workspace_bytes(*args)
+
+
+@pytest.mark.parametrize("kw,want", BAD_MATMUL + [(dict(M=9), tfb.TF_ERR_ARG)],
+                         ids=[str(b[0]) for b in BAD_MATMUL] + ["M=9"])
+def test_gemv_noalloc_rejects(lib, kw, want):
+    """The allocation-free GEMV makes the same checks, before any HIP call."""
+    a = {**MATMUL_OK, **kw}
+    assert lib.tf_w4a16_gemv_noalloc(a["A"], a["packed"], a["C"], a["M"], a["K"], a["N"], a["G"], NULL) == want
