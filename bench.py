@@ -37,7 +37,14 @@ GEMM_SHAPES = [(2048, 4096, 14336), (2048, 14336, 4096)]
 GEMV_SHAPE = (1, 4096, 14336)
 GROUP = 128
 GEMV_REPS = 32
-GEMM_COPIES = 8
+# 17 copies of each prefill weight (17 x 30.7 MB = 522 MB, more than twice the
+# 256 MB MALL), so the timed GEMMs stream their weights from HBM
+GEMM_COPIES = 17
+# The warm-up runs the W steps it is given and then replays the timed graphs
+# until at least this much wall time has passed: the GPU clock takes tens of
+# milliseconds of full load to settle, and a warm-up of a few steps (a few
+# milliseconds) leaves the first timed launches slower.
+WARM_FLOOR_S = 0.3
 PEAK_F16_TFLOPS = 2516.6      # 256 CU x 4096 FLOP/clk x 2.4 GHz (dense fp16 or bf16 MFMA)
 PEAK_HBM_GBS = 8000.0
 COPY_BYTES = 1 << 30
@@ -90,39 +97,93 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(min_seconds=10.0):
-    """The oracle (fp64, numpy/BLAS) timed on the host on whole steps of the
-    same workload: the prefill GEMM pair at full size, then one decode GEMV,
-    repeated until at least `min_seconds` of oracle time have accumulated."""
+CPU_CONFIGS = [
+    # (name, bits, M, K, N, x_std, repeats): the five synthetic workloads;
+    # median of 3 for the small ones, one run for the prefill shapes
+    ("C0 W4 GEMM M=16 K=2048 N=2048", 4, 16, 2048, 2048, 1.0, 3),
+    ("C1 W4 GEMV M=1 K=4096 N=14336", 4, 1, 4096, 14336, 1.0, 3),
+    ("C1 W4 GEMV M=4 K=4096 N=14336", 4, 4, 4096, 14336, 1.0, 3),
+    ("C1 W4 GEMV M=8 K=4096 N=14336", 4, 8, 4096, 14336, 1.0, 3),
+    ("C2 W8 GEMV M=1 K=4096 N=4096", 8, 1, 4096, 4096, 1.0, 3),
+    ("C2 W8 GEMM M=512 K=4096 N=4096", 8, 512, 4096, 4096, 1.0, 3),
+    ("C3a W4 GEMM M=2048 K=4096 N=14336", 4, 2048, 4096, 14336, 1.0, 1),
+    ("C3b W4 GEMM M=2048 K=14336 N=4096", 4, 2048, 14336, 4096, 1.0, 1),
+    ("C4a W4 GEMM M=1024 K=4096 N=32768", 4, 1024, 4096, 32768, 0.5, 1),
+    ("C4b W4 GEMM M=1024 K=32768 N=8192", 4, 1024, 32768, 8192, 0.5, 1),
+]
+ONE_THREAD = ("C0 W4 GEMM M=16 K=2048 N=2048", "C1 W4 GEMV M=1 K=4096 N=14336")
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_times(oracle, d, reps):
+    """Median seconds of the oracle's two stages on one workload: unpack +
+    dequant (Eq. 2 in float64) and the float64 matmul."""
+    td, tm = [], []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        if d["bits"] == 4:
+            q, z = oracle.unpack_w4(d["qweight"]), oracle.unpack_w4(d["qzeros"])
+        else:
+            q, z = d["qweight"], d["zeros"]
+        w = oracle.dequant(q, z, d["s"], GROUP)
+        t1 = time.perf_counter()
+        y = oracle.matmul(d["x"], w)
+        t2 = time.perf_counter()
+        assert np.isfinite(y).all()
+        del w, y, q, z
+        td.append(t1 - t0)
+        tm.append(t2 - t1)
+    return float(np.median(td)), float(np.median(tm))
+
+
+def cpu_baseline():
+    """The oracle (numpy: unpack, Eq. 2 in float64, float64 BLAS matmul) timed
+    on this host on every synthetic workload: dequant and matmul separately,
+    median of 3 runs for the small workloads and one run for the prefill
+    shapes, with all BLAS threads; a one-thread figure for the M=16 GEMM and
+    the M=1 GEMV.  `value` is the prefill GEMM pair's rate (the headline
+    metric's workload): 2*M*N*K of both shapes over their oracle time."""
     import oracle
     from paper_2606_11357_amd.synth import make_inputs
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count()
-    gemm_in = [make_inputs(4, M, K, N, group=GROUP, seed=0) for (M, K, N) in GEMM_SHAPES]
-    M1, K1, N1 = GEMV_SHAPE
-    gemv_in = make_inputs(4, M1, K1, N1, group=GROUP, seed=0)
-    t_gemm = t_gemv = 0.0
-    reps = 0
-    while t_gemm + t_gemv < min_seconds:
-        for d in gemm_in:
-            t0 = time.perf_counter()
-            y = oracle.w4a16(d["x"], d["qweight"], d["qzeros"], d["s"], GROUP)
-            t_gemm += time.perf_counter() - t0
-            assert np.isfinite(y).all()
-        t0 = time.perf_counter()
-        oracle.w4a16(gemv_in["x"], gemv_in["qweight"], gemv_in["qzeros"], gemv_in["s"], GROUP)
-        t_gemv += time.perf_counter() - t0
-        reps += 1
-    flops = reps * sum(2.0 * M * N * K for (M, K, N) in GEMM_SHAPES)
-    return {"value": round(flops / t_gemm / 1e12, 4), "unit": "TFLOP/s", "cores": int(threads),
-            "kind": "oracle", "seconds": round(t_gemm + t_gemv, 3), "steps": reps,
-            "gemv_GBps": round(reps * algo_bytes_w4(K1, N1) / t_gemv / 1e9, 3),
-            "sample": "%d whole steps: the prefill GEMM pair (M=2048; K,N = 4096,14336 and "
-                      "14336,4096) and one M=1 GEMV each; oracle = unpack + fp64 dequant + "
-                      "fp64 BLAS matmul; value from the GEMM time" % reps}
+    from threadpoolctl import threadpool_info, threadpool_limits
+    threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    per = {}
+    t_total = 0.0
+    for name, bits, M, K, N, xstd, reps in CPU_CONFIGS:
+        d = make_inputs(bits, M, K, N, group=GROUP, seed=0, x_std=xstd)
+        tdq, tmm = _oracle_times(oracle, d, reps)
+        flops = 2.0 * M * N * K
+        rec = {"dequant_s": round(tdq, 4), "matmul_s": round(tmm, 4), "runs": reps,
+               "GFLOP/s": round(flops / (tdq + tmm) / 1e9, 3),
+               "GB/s": round(algo_bytes(bits, K, N) / (tdq + tmm) / 1e9, 3)}
+        t_total += reps * (tdq + tmm)
+        if name in ONE_THREAD:
+            with threadpool_limits(limits=1):
+                t1d, t1m = _oracle_times(oracle, d, reps)
+            rec["one_thread"] = {"dequant_s": round(t1d, 4), "matmul_s": round(t1m, 4),
+                                 "GFLOP/s": round(flops / (t1d + t1m) / 1e9, 3)}
+            t_total += reps * (t1d + t1m)
+        per[name] = rec
+        del d
+    pair = [per[n] for n in ("C3a W4 GEMM M=2048 K=4096 N=14336", "C3b W4 GEMM M=2048 K=14336 N=4096")]
+    t_pair = sum(r["dequant_s"] + r["matmul_s"] for r in pair)
+    flops_pair = sum(2.0 * M * N * K for (M, K, N) in GEMM_SHAPES)
+    return {"value": round(flops_pair / t_pair / 1e12, 4), "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle", "cpu_model": _cpu_model(), "os_cpu_count": os.cpu_count(),
+            "blas_threads": int(threads), "seconds": round(t_total, 2),
+            "sample": "every synthetic workload once through the oracle (unpack + float64 dequant, "
+                      "then float64 BLAS matmul; median of 3 runs below M=2048, one run at M>=1024); value "
+                      "= the M=2048 prefill pair, both stages",
+            "per_config": per}
 
 
 def calibrate_copy(torch):
@@ -233,11 +294,45 @@ def graph_time_us(torch, fn, reps):
     return e0.elapsed_time(e1) * 1e3 / (3 * reps)
 
 
+def read_ceiling(torch, nbytes, reps=64):
+    """Streaming-read ceiling for a launch that reads `nbytes` once: the read
+    probe (paper_2606_11357_amd/probe, a kernel that only loads) over a sweep
+    of launch shapes, rotating over enough buffers to exceed 512 MB so every
+    launch reads HBM; HIP-graph replay timing.  Returns one record per shape,
+    fastest first."""
+    import ctypes
+    from paper_2606_11357_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    lib.tf_probe_read.restype = ctypes.c_int
+    lib.tf_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                  ctypes.c_void_p, ctypes.c_void_p]
+    dev = torch.device("cuda:0")
+    nbytes = nbytes // 16 * 16
+    ncopy = -(-(512 << 20) // nbytes)
+    bufs = [torch.ones(nbytes, device=dev, dtype=torch.uint8) for _ in range(ncopy)]
+    sink = torch.zeros(4, device=dev, dtype=torch.int32)
+    out = []
+    for grid, block, unroll in ((224, 1024, 8), (224, 1024, 4), (256, 1024, 8), (256, 1024, 4), (256, 512, 16),
+                                (512, 512, 8), (512, 1024, 4), (1024, 256, 8), (1024, 256, 16), (2048, 256, 4),
+                                (2048, 256, 8), (4096, 256, 2)):
+        def launch(i, g=grid, b=block, u=unroll):
+            rc = lib.tf_probe_read(ctypes.c_void_p(bufs[i % ncopy].data_ptr()), nbytes, g, b, u,
+                                   ctypes.c_void_p(sink.data_ptr()),
+                                   ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+            assert rc == 0, rc
+        us = graph_time_us(torch, launch, reps)
+        out.append({"grid": grid, "block": block, "unroll": unroll, "us_per_launch": round(us, 3),
+                    "read_GB/s": round(nbytes / us / 1e3, 1)})
+    del bufs
+    return sorted(out, key=lambda r: r["us_per_launch"])
+
+
 def context(torch):
     """Achievable-ceiling references, not targets: torch.matmul in fp16 (the
     weights already dequantized to a dense fp16 [K, N]) on the two prefill
-    shapes, and a device copy of the decode GEMV's packed-weight byte count,
-    rotating over sources so it streams from HBM."""
+    shapes; the streaming-read ceiling for the decode GEMV's byte count (a
+    kernel that only reads, over a sweep of launch shapes); and a device copy
+    of the same byte count, rotating over sources so it streams from HBM."""
     dev = torch.device("cuda:0")
     gen = torch.Generator(device=dev).manual_seed(0)
     for (M, K, N) in GEMM_SHAPES:
@@ -250,6 +345,12 @@ def context(torch):
                           "TFLOP/s": round(2.0 * M * N * K / us / 1e6, 2)}), flush=True)
         del a, ws, out
     nbytes = algo_bytes_w4(GEMV_SHAPE[1], GEMV_SHAPE[2])
+    for bytes_, what in ((nbytes, "the decode GEMV's metric bytes (K=4096 N=14336 W4)"),
+                         (256 << 20, "256 MiB (asymptotic rate)")):
+        shapes = read_ceiling(torch, bytes_)
+        print(json.dumps({"reference": "streaming read (read-only probe kernel) of " + what, "bytes_read": bytes_,
+                          "best": shapes[0], "gemv_like_grid_224x1024": [r for r in shapes if r["grid"] == 224][0],
+                          "all_shapes": shapes}), flush=True)
     ncopy = -(-(512 << 20) // nbytes)
     bufs = [torch.empty(nbytes, device=dev, dtype=torch.uint8) for _ in range(ncopy)]
     dst = torch.empty(nbytes, device=dev, dtype=torch.uint8)
@@ -410,8 +511,8 @@ def main():
                           d["K"], d["N"], GROUP)
 
     # ---- inputs (offline: generation + pack are outside the timed region);
-    # GEMM_COPIES copies of each prefill weight (about 490 MB in all, more than
-    # the 256 MB MALL), so the GEMMs stream their weights from HBM
+    # GEMM_COPIES copies of each prefill weight (522 MB per shape, more than
+    # twice the 256 MB MALL), so the GEMMs stream their weights from HBM
     gemm = []
     for (M, K, N) in GEMM_SHAPES:
         d = make_inputs(4, M, K, N, group=GROUP, seed=0)
@@ -455,12 +556,23 @@ def main():
         for s in range(args.steps):
             gemv_batch()
     torch.cuda.synchronize()
-    # The W warm-up steps run right before the timed region, so the GPU
-    # enters it busy (capture above leaves it idle, and clocks drop then).
+    # Warm-up, right before the timed region (capture above leaves the GPU
+    # idle, and its clock drops): the W steps as given, eagerly, then replays
+    # of the timed graphs until WARM_FLOOR_S of wall time have passed.
+    t_w = time.perf_counter()
     for s in range(args.warmup):
         for g in gemm:
             gemm_one(g, s % GEMM_COPIES)
         gemv_batch()
+    torch.cuda.synchronize()
+    warm_replays = 0
+    while time.perf_counter() - t_w < WARM_FLOOR_S:
+        for cg in graphs:
+            cg.replay()
+        g_gemv.replay()
+        torch.cuda.synchronize()
+        warm_replays += 1
+    warm_s = time.perf_counter() - t_w
 
     # The timed region holds the K steps' work grouped by kernel: the K
     # launches of each prefill shape back to back (weights stream from HBM,
@@ -515,8 +627,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(tflops / PEAK_F16_TFLOPS, 4),
             "traffic": recorded_traffic("tf_gemm256.hip"),
-            "kernel": "gemm256_kernel<4,1,false> (K=4096 N=14336: whole 256x256 tiles; "
-                      "K=14336 N=4096: stream-K over 256 blocks)",
+            "kernel": "gemm256_kernel (the launch plan of each shape is named by TF_LOG=1 and the profiles)",
         },
         "gemv": {
             "value": round(gemv_gbs, 1),
@@ -525,11 +636,14 @@ def main():
             "bytes_per_launch": gemv_bytes,
             "roofline": {"bound": "hbm", "achieved": round(gemv_gbs, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(gemv_gbs / PEAK_HBM_GBS, 4),
-                         "traffic": recorded_traffic("tf_gemv.hip"),
-                         "kernel": "gemv_kernel<4,1,16,4,8,false> (one-round form)"},
+                         "traffic": recorded_traffic("tf_gemv.hip"), "kernel": "gemv_kernel"},
         },
         "gemm_ms_per_step": round(gemm_ms, 4),
         "gemm_us_per_shape": {f"K={K},N={N}": round(t * 1e3, 2) for (M, K, N), t in zip(GEMM_SHAPES, shape_ms)},
+        "warmup_s": round(warm_s, 3),
+        "warmup_graph_replays": warm_replays,
+        "timing": "HIP events on the launch stream around one graph replay per phase (K launches each); "
+                  "value = 2*M*N*K of both prefill shapes over their summed mean launch time",
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline()
