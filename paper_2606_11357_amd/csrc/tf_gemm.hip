@@ -12,8 +12,8 @@
 //    4.1.1 and 4.3: dequantize a weight tile once, reuse it for every
 //    activation row).  The next chunk's atoms and metadata are loaded a whole
 //    chunk ahead; the group constants are formed once per chunk.
-//  - A (fp16) goes global -> registers -> LDS through three XOR-swizzled LDS
-//    buffers: the loads for step s+2 leave while step s is multiplied and are
+//  - A (fp16) goes global -> registers -> LDS through three LDS buffers (16-row
+//    blocks chunk-major): the loads for step s+2 leave while step s is multiplied and are
 //    written to LDS one step later, so each load has more than a step to land;
 //    one barrier per step.
 //  - Tiles are numbered so that each XCD (workgroups are dealt round-robin
@@ -103,16 +103,18 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(
 #pragma unroll
         for (int t = 0; t < 4; ++t) acc[i][t] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-    // ---- A: 128 rows x 32 halves per step = 512 chunks, 2 per thread.  Rows
-    // past M read row M-1 instead (in bounds; those rows are never stored).
+    // ---- A: 128 rows x 32 halves per step = 512 chunks, 2 per thread; thread
+    // chunk idx is the one LDS slot idx holds, so each wave stores 1 KB of
+    // consecutive slots.  Rows past M read row M-1 instead (in bounds; those
+    // rows are never stored).
     const uint16_t* arow[2];
     int aslot[2];
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
         const int idx = tid + kGemmThreads * r;
-        const int64_t grow = min<int64_t>(row0 + (idx >> 2), (int64_t)M - 1);
-        arow[r] = A + grow * K + (idx & 3) * 8 + (int64_t)st0 * kBK;
-        aslot[r] = a_slot(idx >> 2, idx & 3);
+        const int64_t grow = min<int64_t>(row0 + lds_a_row(idx), (int64_t)M - 1);
+        arow[r] = A + grow * K + lds_a_chunk(idx) * 8 + (int64_t)st0 * kBK;
+        aslot[r] = idx;
     }
     const int steps = chunks * CS0;            // one 32-row step per atom
     auto load_a = [&](int step, u32x4 (&av)[2]) {
@@ -356,7 +358,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_generic(
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
             const int idx = tid + kGemmThreads * r;
-            const int row = idx >> 2, ch = idx & 3;
+            const int row = lds_a_row(idx), ch = lds_a_chunk(idx);   // the chunk slot idx holds
             const int64_t grow = row0 + row;
             av[r] = grow < M ? *reinterpret_cast<const u32x4*>(A + grow * K + (int64_t)a * kBK1 + ch * 8)
                              : u32x4{0u, 0u, 0u, 0u};
@@ -396,7 +398,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel_generic(
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
             const int idx = tid + kGemmThreads * r;
-            As[a_swz1(idx >> 2, idx & 3)] = av[r];
+            As[idx] = av[r];
         }
         __syncthreads();
 #pragma unroll

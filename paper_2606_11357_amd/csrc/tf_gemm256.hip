@@ -9,9 +9,9 @@
 // one vector-ALU instruction per v_mfma_f32_16x16x32_f16, which the SIMD
 // issues while the matrix core works (Sections 4.1.1 and 4.3: dequantize each
 // weight tile once and reuse it for every activation row).
-//  - A (fp16) goes global -> registers -> LDS through three XOR-swizzled
-//    buffers of 256 rows x 32 halves; loads for step s+1 leave at the start of
-//    step s and are written to LDS at its end; one barrier per step.
+//  - A (fp16) goes global -> LDS (direct loads) through four
+//    buffers of 256 rows x 32 halves (each 16-row block chunk-major, so every
+//    fragment read is 1 KB of consecutive bytes); one barrier per step.
 //  - The wave's packed atoms are loaded three steps ahead into a register
 //    ring and dequantized one step ahead, straight into the B-operand layout.
 //  - Loads go through buffer resources: the step advances a scalar offset,
@@ -152,14 +152,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
 
     // A step tile (256 rows x 32 halves = 1024 16-byte slots) arrives by four
     // direct loads per thread; load r of wave w fills slots (4 w + r) * 64 +
-    // lane (a direct load writes lane l's 16 bytes at its base + 16 l), so
-    // each lane fetches the A chunk that belongs in its slot: slot X holds
-    // row X / 4, chunk (X % 4) ^ lds_chunk_swz(row) (the inverse of a_slot).
+    // lane (a direct load writes lane l's 16 bytes at its base + 16 l), i.e.
+    // the 16-row block 4 w + r, so each lane fetches the A chunk that belongs
+    // in its slot (lds_a_row / lds_a_chunk, the inverse of a_slot).
     uint32_t avoff[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int x = (4 * wave + r) * 64 + lane;
-        const int row = x >> 2, chk = (x & 3) ^ lds_chunk_swz(row);
+        const int row = lds_a_row(x), chk = lds_a_chunk(x);
         avoff[r] = (uint32_t)row * (uint32_t)K * 2u + (uint32_t)chk * 16u;
     }
     auto read_a = [&](int buf, int i) { return abuf(buf)[a_slot(16 * i + c, kg)]; };

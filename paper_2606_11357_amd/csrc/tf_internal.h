@@ -291,17 +291,20 @@ __device__ __forceinline__ half8_t dq_w8_dwords(uint32_t w0, uint32_t w1, uint32
 }
 
 // 16-byte LDS slot of chunk `ch` (0..3) of activation row `row` in a tile of
-// 64-byte rows (32 fp16 / bf16 values of K per row).  The matrix-core kernels
-// read one chunk of 16 consecutive rows per quarter of a wavefront
-// (ds_read_b128: lane c of the quarter reads row r0 + c).  XOR-ing the chunk
-// with ((row >> 1) ^ (row >> 3)) & 3 puts every 8 consecutive rows of one
-// chunk in 8 distinct 16-byte slots modulo 8, and every 16 in 16 distinct
-// slots modulo 16, so no two lanes served together share an LDS bank (ds_read_b128
-// measured on MI355X at the rate of a contiguous read; the XOR with row bits
-// 2..3 alone, distinct only modulo 16, ran 36% slower).  The XOR is its own
-// inverse: chunk ^ f(row) also maps a slot back to its chunk.
-__device__ __forceinline__ int lds_chunk_swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
-__device__ __forceinline__ int lds_a_slot(int row, int ch) { return row * 4 + (ch ^ lds_chunk_swz(row)); }
+// 64-byte rows (32 fp16 / bf16 values of K per row), a whole number of 16-row
+// blocks.  Each 16-row block is stored chunk-major: chunk 0 of its 16 rows,
+// then chunk 1, and so on.  The matrix-core kernels read one 16-row block per
+// ds_read_b128 (lane c of quarter kg reads row r0 + c, chunk kg), so the 64
+// lanes of a wavefront read 1 KB of consecutive bytes, which the LDS serves
+// without bank conflicts; the block's writers (a direct load or a store of
+// 64 lanes) likewise cover 1 KB of consecutive slots.  (Measured on MI355X
+// with a read-only probe: the former layout, chunks XOR-swizzled inside each
+// row, took 4 bank-conflict cycles per ds_read_b128 and ran 68% slower than
+// this one.)
+__device__ __forceinline__ int lds_a_slot(int row, int ch) { return ((row >> 4) << 6) + (ch << 4) + (row & 15); }
+// The row and chunk that slot x holds (the inverse of lds_a_slot).
+__device__ __forceinline__ int lds_a_row(int x) { return ((x >> 6) << 4) + (x & 15); }
+__device__ __forceinline__ int lds_a_chunk(int x) { return (x >> 4) & 3; }
 
 // ---------------------------------------------------------------------------
 // BF16 activations and scales (Sections 2.2 and 4.3: the paper's kernels take
