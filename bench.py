@@ -94,6 +94,10 @@ def parse():
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the step, time every synthetic workload configuration "
                          "(one JSON line each)")
+    ap.add_argument("--workload", default=None,
+                    help="with --sweep: only this workload (a name of synth.WORKLOADS)")
+    ap.add_argument("--dtype", default=None, choices=("f16", "bf16"),
+                    help="with --sweep or --mlp: only this activation dtype")
     return ap.parse_args()
 
 
@@ -203,7 +207,7 @@ def algo_bytes(bits, K, N, G=GROUP):
     return K * N + (K // G) * N * 2 + (K // G) * N
 
 
-def sweep(torch, tf, make_inputs, reps=50, dtypes=("f16", "bf16")):
+def sweep(torch, tf, make_inputs, reps=50, dtypes=("f16", "bf16"), only=None):
     """Every workload of synth.WORKLOADS, with fp16 and with BF16 activations
     and scales: HIP-event time per launch over 3 replays of a graph of `reps`
     launches rotating over enough distinct copies of the packed weight that
@@ -213,8 +217,12 @@ def sweep(torch, tf, make_inputs, reps=50, dtypes=("f16", "bf16")):
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
     up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    if only is not None and only not in WORKLOADS:
+        raise SystemExit(f"unknown workload {only}; one of {', '.join(WORKLOADS)}")
     for dt in dtypes:
         for name, (bits, Ms, K, N, xstd) in WORKLOADS.items():
+            if only is not None and name != only:
+                continue
             for M in Ms:
                 if dt == "bf16":
                     d = make_inputs_bf16(bits, M, K, N, group=GROUP, seed=0, x_std=xstd)
@@ -491,14 +499,15 @@ def main():
         context(torch)
         return
     tf.load()
+    dtypes = (args.dtype,) if args.dtype else ("f16", "bf16")
     if args.sweep:
-        sweep(torch, tf, make_inputs)
+        sweep(torch, tf, make_inputs, dtypes=dtypes, only=args.workload)
         return
     if args.msweep:
         msweep(torch, tf, make_inputs)
         return
     if args.mlp:
-        mlp(torch, tf, make_inputs)
+        mlp(torch, tf, make_inputs, dtypes=dtypes)
         return
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
