@@ -9,9 +9,15 @@
 // one vector-ALU instruction per v_mfma_f32_16x16x32_f16, which the SIMD
 // issues while the matrix core works (Sections 4.1.1 and 4.3: dequantize each
 // weight tile once and reuse it for every activation row).
-//  - A (fp16) goes global -> LDS (direct loads) through four
-//    buffers of 256 rows x 32 halves (each 16-row block chunk-major, so every
-//    fragment read is 1 KB of consecutive bytes); one barrier per step.
+//  - A (fp16) goes global -> LDS by direct loads, two K steps at a time:
+//    three buffers of 256 rows x 64 halves (128 bytes per row, so each direct
+//    load brings eight whole rows of cache lines), rows XOR-swizzled in 16-byte
+//    chunks so fragment reads are free of bank conflicts; one barrier per step.
+//  - A fragments are read from LDS in two bursts per step, a half step ahead
+//    of their use, and the dequantization runs in the parts of the step where
+//    no LDS data is returning: measured on MI355X, LDS reads interleaved one
+//    by one with vector-ALU work stall the matrix core far more than the same
+//    work kept apart.
 //  - The wave's packed atoms are loaded three steps ahead into a register
 //    ring and dequantized one step ahead, straight into the B-operand layout.
 //  - Loads go through buffer resources: the step advances a scalar offset,
@@ -29,14 +35,45 @@ namespace {
 constexpr int kBM = 256, kBN = 256, kBK = 32;
 constexpr int kThreads = 256;
 constexpr int kXcds = 8;
-constexpr int kABufs = 4;                // = steps per chunk: buffer index j is static
 constexpr int kCS = 4;                 // steps per 128-row chunk (atom ring size)
+constexpr int kPairK = 2 * kBK;        // K rows per A buffer (two steps)
+constexpr int kPairBufs = 3;           // A buffers: the pair being read, the next, one landing
+constexpr int kPairBytes = kBM * kPairK * 2;   // 32 KB
+constexpr int kRowBytes = kPairK * 2;  // 128 bytes of A per row per buffer
 constexpr int kRB = kBM / 16;          // 16-row blocks per wave
 constexpr int kSkMinUnits = 8;         // fewest K chunks per block when every tile is split
 
-// 16-byte LDS slot of chunk `ch` (0..3) of A row `row` (64-byte rows; see
-// lds_a_slot).
-__device__ __forceinline__ int a_slot(int row, int ch) { return lds_a_slot(row, ch); }
+// A buffer layout: row r of the tile at byte r * 128; its 16-byte chunk of
+// halves 8 l .. 8 l + 7 (l = 0..7) at position l ^ a_swz(r).  A fragment read
+// covers 16 rows (16 i .. 16 i + 15) at one logical chunk: the swizzle spreads
+// them over all 64 banks (16 lanes served per pass) and over all 32 banks of
+// each half (8 lanes per pass).
+__device__ __forceinline__ int a_swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
+// 16-byte LDS read issued as an asm statement, so the compiler neither waits
+// for the direct loads in flight into the other A buffers (it cannot tell the
+// buffers of one array apart) nor for the read itself: the kernel waits for
+// its reads explicitly (lds_wait) before their first use.
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read16_at(uint32_t addr) {
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+    return v;
+}
+// fragment of row block i (16 rows x 128 bytes = 2 KB apart); i is a
+// constant once the step's slot loop is unrolled
+__device__ __forceinline__ u32x4 lds_read_block(uint32_t addr, int i) {
+    switch (i) {
+#define TF_BLOCK(n) \
+    case n: return lds_read16_at<(n) * 16 * kRowBytes>(addr);
+        TF_BLOCK(0) TF_BLOCK(1) TF_BLOCK(2) TF_BLOCK(3) TF_BLOCK(4) TF_BLOCK(5) TF_BLOCK(6) TF_BLOCK(7)
+        TF_BLOCK(8) TF_BLOCK(9) TF_BLOCK(10) TF_BLOCK(11) TF_BLOCK(12) TF_BLOCK(13) TF_BLOCK(14) TF_BLOCK(15)
+#undef TF_BLOCK
+        default: return lds_read16_at<0>(addr);
+    }
+}
+// every LDS read of this wave has returned
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 __device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
@@ -115,15 +152,23 @@ __device__ __forceinline__ int sk_owner(int64_t u, int G, int U) {   // block wh
 }
 __device__ __forceinline__ int sk_begin(int v, int G, int U) { return (int)((int64_t)v * U / G); }
 
-// Slots of a K step's 64 that carry dequantization micro-steps: 4 .. 63.
-// fp16 needs at most 52 micro-steps per step (one per slot from slot 4);
-// bf16 needs 88 (4-bit) or 80 (8-bit), spread one or two per slot.
-constexpr int kDqFirstSlot = 4, kDqSlots = 64 - kDqFirstSlot;
-// first micro-step of slot q (q = kDqFirstSlot .. 64) when R are placed
-constexpr int dq_slot_begin(int q, int R) {
-    return R <= kDqSlots ? (q - kDqFirstSlot < R ? q - kDqFirstSlot : R)
-                         : (q - kDqFirstSlot) * R / kDqSlots;
+// Slots of a K step's 64 that carry dequantization micro-steps: two windows,
+// [W, 32) and [W + 32, 64), after the two LDS read bursts (slots 0..7 and
+// 32..39) have returned.  fp16 (52 or 48 micro-steps) uses W = 16, one or two
+// per slot; bf16 (92 or 80) uses W = 8, at most two per slot.
+template <bool BF>
+constexpr int dq_window() { return BF ? 8 : 16; }
+template <bool BF>
+constexpr int dq_slots() { return 2 * (32 - dq_window<BF>()); }
+template <bool BF>
+constexpr int dq_index(int q) {
+    return (q & 31) < dq_window<BF>() ? -1 : (q >> 5) * (32 - dq_window<BF>()) + (q & 31) - dq_window<BF>();
 }
+// micro-steps [dq_slot_begin, dq_slot_end) of R go to slot q
+template <bool BF>
+constexpr int dq_slot_begin(int q, int R) { return dq_index<BF>(q) < 0 ? 0 : dq_index<BF>(q) * R / dq_slots<BF>(); }
+template <bool BF>
+constexpr int dq_slot_end(int q, int R) { return dq_index<BF>(q) < 0 ? 0 : (dq_index<BF>(q) + 1) * R / dq_slots<BF>(); }
 
 template <int BITS, int MPC, bool BF>
 __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
@@ -134,11 +179,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     constexpr int T = PW / 16;                 // columns per lane per atom
     constexpr int PANELS = 64 / PW;            // panels per wave
     constexpr int SPG = kCS / MPC;             // steps per metadata group
-    // One array per A buffer, so the compiler can tell the buffers apart when
-    // it orders LDS reads after the direct loads into another buffer.
-    __shared__ __align__(16) u32x4 As0[kBM * kBK / 8], As1[kBM * kBK / 8], As2[kBM * kBK / 8],
-        As3[kBM * kBK / 8];
-    auto abuf = [&](int j) -> u32x4* { return j == 0 ? As0 : j == 1 ? As1 : j == 2 ? As2 : As3; };
+    __shared__ __align__(16) uint8_t As[kPairBufs * kPairBytes];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -148,21 +189,29 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     const int chunks = steps / kCS;            // the launcher requires K % 128 == 0
     constexpr int kDqSteps = dq_steps<BF, BITS>();
     constexpr int kDqTotal = 4 * kDqSteps;     // micro-steps per K step
-    static_assert(kDqTotal <= 2 * kDqSlots, "at most two micro-steps per slot");
+    static_assert(kDqTotal <= 2 * dq_slots<BF>(), "at most two micro-steps per slot");
 
-    // A step tile (256 rows x 32 halves = 1024 16-byte slots) arrives by four
-    // direct loads per thread; load r of wave w fills slots (4 w + r) * 64 +
-    // lane (a direct load writes lane l's 16 bytes at its base + 16 l), i.e.
-    // the 16-row block 4 w + r, so each lane fetches the A chunk that belongs
-    // in its slot (lds_a_row / lds_a_chunk, the inverse of a_slot).
-    uint32_t avoff[4];
+    // An A buffer (256 rows x 64 halves, 32 KB) arrives by eight direct loads
+    // per thread, four in each of two steps; load r of wave w fills bytes
+    // (8 w + r) KB .. + 1 KB (a direct load writes lane l's 16 bytes at its
+    // base + 16 l), i.e. rows 64 w + 8 r .. + 7, eight lanes per row, so each
+    // lane fetches the A chunk that belongs at its position (the inverse of
+    // a_swz): eight whole 128-byte rows of A per load.
+    uint32_t avoff[8];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int x = (4 * wave + r) * 64 + lane;
-        const int row = lds_a_row(x), chk = lds_a_chunk(x);
-        avoff[r] = (uint32_t)row * (uint32_t)K * 2u + (uint32_t)chk * 16u;
+    for (int r = 0; r < 8; ++r) {
+        const int row = 64 * wave + 8 * r + (lane >> 3);
+        const int lc = (lane & 7) ^ a_swz(row);
+        avoff[r] = (uint32_t)row * (uint32_t)K * 2u + (uint32_t)lc * 16u;
     }
-    auto read_a = [&](int buf, int i) { return abuf(buf)[a_slot(16 * i + c, kg)]; };
+    // Fragment of row block i (rows 16 i + c, halves 8 kg .. + 7 of the step):
+    // lane byte offset inside a buffer for an even (first) and an odd step;
+    // the block adds 2 KB per i as an immediate offset.
+    const uint32_t a_lds = (uint32_t)reinterpret_cast<uintptr_t>(As);
+    uint32_t a_lane[2];
+#pragma unroll
+    for (int odd = 0; odd < 2; ++odd)
+        a_lane[odd] = a_lds + (uint32_t)(c * kRowBytes + ((kg + 4 * odd) ^ a_swz(c)) * 16);
     struct Meta {
         uint32_t s[MPC][PANELS][(T + 1) / 2];   // T fp16 scales per group and panel
         uint32_t z[MPC][PANELS];                // T zero-point bytes
@@ -212,7 +261,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     // row m = 16 i + c, columns n = 16 t + 4 kg + 0..3 of the wave's tile.
     // The caller has made sure no wave still reads the A buffers underneath.
     auto store_tile = [&](int64_t row0, int64_t col0, auto&& get_block) {
-        uint8_t* stage = reinterpret_cast<uint8_t*>(As0) + wave * 4096;
+        uint8_t* stage = As + wave * 4096;
         constexpr int kStageRow = 144;
         const bool interior = row0 + kBM <= M && col0 + 64 <= N;
         const int rr = lane >> 3, cc = lane & 7;      // read-back: row rr (+8), 16-byte chunk cc
@@ -256,14 +305,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         row0_out = row0;
         col0_out = col0;
 
-        // A: the tile's rows as one buffer (rows past M read as zero); 256 rows
-        // x 32 halves per step = 1024 16-byte chunks, 4 per thread.
+        // A: the tile's rows as one buffer (rows past M read as zero); a pair
+        // of steps (256 rows x 64 halves) = 32 direct loads of 1 KB, 8 per
+        // thread.
         const int rows = (int)min<int64_t>(kBM, (int64_t)M - row0);
         const __amdgpu_buffer_rsrc_t a_rsrc = make_rsrc(A + row0 * K, (uint32_t)rows * (uint32_t)K * 2u);
-        auto dma_a = [&](int step, int buf, int r) {      // direct load r of step's A tile
-            const uint32_t soff = (uint32_t)min(step, steps - 1) * (kBK * 2);
+        const int pairs = steps / 2;
+        auto dma_a = [&](int pair, uint32_t buf, int r) {  // direct load r (0..7) of a pair's A into buffer byte offset buf
+            const uint32_t soff = (uint32_t)min(pair, pairs - 1) * kRowBytes;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                a_rsrc, (__attribute__((address_space(3))) void*)(abuf(buf) + (4 * wave + r) * 64), 16,
+                a_rsrc, (__attribute__((address_space(3))) void*)(As + buf + (8 * wave + r) * 1024), 16,
                 avoff[r], soff, 0, 0);
         };
         // B: packed panels and metadata as buffers; a panel past N is an
@@ -311,16 +362,20 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
 #pragma unroll
             for (int t = 0; t < 4; ++t) acc[i][t] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-        // Prologue (s0 = first step): A of steps s0..s0+2 into LDS buffers
-        // 0..2; atoms of steps s0..s0+3 and metadata of the first two chunks
-        // requested; B operands of step s0; everything landed, then the first
-        // A fragments of step s0 read.  Buffer j holds the A of a step = j
-        // mod 4 (s0 is a multiple of 4).
+        // Prologue (s0 = first step, pair p0 = s0 / 2): A of pairs p0, p0+1
+        // (steps s0..s0+3) into buffers b0, b1; atoms of steps s0..s0+3 and
+        // metadata of the first two chunks requested; B operands of step s0;
+        // everything landed, then the A fragments of blocks 0..7 of step s0
+        // read.  Within a chunk ch the steps use buffers b0, b0, b1, b1 (pairs
+        // 2 ch, 2 ch + 1); the direct loads of pair 2 ch + 2 go to b2 during
+        // its first two steps, those of pair 2 ch + 3 to b0 (free once its
+        // second step is done) during the last two; then the three rotate.
         const int s0 = c0 * kCS;
+        uint32_t b0 = 0, b1 = kPairBytes, b2 = 2 * kPairBytes;
 #pragma unroll
-        for (int b = 0; b < 3; ++b)
+        for (int r = 0; r < 8; ++r) dma_a(s0 / 2, b0, r);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) dma_a(s0 + b, b, r);
+        for (int r = 0; r < 8; ++r) dma_a(s0 / 2 + 1, b1, r);
 #pragma unroll
         for (int j = 0; j < kCS; ++j) load_atom(s0 + j, ring[j]);
         Meta mcur, mnext;
@@ -332,43 +387,46 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         dequant(ring[0], kc, bop);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
-        // A fragment ring: block i of every step uses entry i % 8 (16 blocks
-        // per step, so the pattern repeats exactly from step to step); reads
-        // run four blocks ahead.
-        constexpr int kLead = 4, kRing = 8;
-        u32x4 af[kRing];
+        // A fragments: block i of every step in af[i]; blocks 8..15 are read
+        // at the start of their step, blocks 0..7 half a step before theirs.
+        u32x4 af[kRB];
 #pragma unroll
-        for (int i = 0; i < kLead; ++i) af[i] = read_a(0, i);
+        for (int i = 0; i < kRB / 2; ++i) af[i] = lds_read_block(a_lane[0] + b0, i);
+        lds_wait();
         mfma_hazard_gap();
 
         // One K step s (j = s mod 4), as 64 MFMA slots (row block i = slot / 4,
         // column block t = slot % 4), each followed by at most one other
         // instruction group, fixed by scheduling fences:
-        //   slot 0        loads of the atoms for step s+4 (into the ring slot
-        //                 of step s, whose operands were formed during s-1)
-        //   slots 2+4r    direct load r (0..3) of A of step s+3 into buffer
-        //                 (s+3) % 4, last read during step s-1 (before the
-        //                 previous barrier)
-        //   slots 4i      A fragment of row block i + 4 from LDS (eight-entry
-        //                 ring, so each LDS read has four blocks to land); for
-        //                 i = 12..15 fragment i - 12 of step s+1 instead
-        //                 (written before the previous barrier)
-        //   slots 4..     the dequantization micro-steps of step s+1's B
+        //   slot 0        wait for this step's blocks 0..7 (read half a step
+        //                 ago); loads of the atoms for step s+4 (into the ring
+        //                 slot of step s, whose operands were formed during s-1)
+        //   slots 0..7    A fragments of blocks 8..15 of step s
+        //   slot 32       wait for them
+        //   slots 32..39  A fragments of blocks 0..7 of step s+1
+        //   slots 16+4r   direct load r (0..3) of half of the A pair two ahead
+        //   [W, 32), [W + 32, 64)
+        //                 the dequantization micro-steps of step s+1's B
         //                 operands, one vector instruction each, issued while
-        //                 the matrix core works: fp16 52 (4-bit) or 48 (8-bit),
-        //                 one per slot from slot 4; bf16 88 or 80, one or two
-        //                 per slot over slots 4..63
-        // then one barrier, after this wave's direct loads of step s+2 (issued
-        // during step s-1) have landed.
+        //                 the matrix core works and no LDS data returns
+        // then one barrier, after this wave's loads issued during step s-1
+        // (the direct loads of the pair the next step may read) have landed.
         for (int ch = c0; ch < c1; ++ch) {
 #pragma unroll
             for (int j = 0; j < kCS; ++j) {
                 const int step = ch * kCS + j;
-                const int buf = j;                        // step % kABufs (s0 % 4 == 0)
+                const int odd = j & 1;
+                const uint32_t bcur = j < 2 ? b0 : b1;                    // this step's pair
+                const uint32_t bnxt = j == 0 ? b0 : (j == 3 ? b2 : b1);   // step s+1's pair
+                const uint32_t bdma = j < 2 ? b2 : b0;                    // pair 2 ch + 2 + j / 2
+                const int dpair = 2 * ch + 2 + (j >> 1);
                 if (j == kCS - 1) {
-                    mcur = mnext;                         // first group of the next chunk
+                    // constants of the next chunk's first group, from metadata
+                    // that landed a chunk ago, formed before its registers
+                    // are reloaded (a load into live registers would wait)
+                    make_consts(mnext, 0, kc);
+                    if constexpr (MPC > 1) mcur = mnext;
                     load_meta(ch + 2, mnext);
-                    make_consts(mcur, 0, kc);
                 } else if ((j + 1) % SPG == 0) {
                     make_consts(mcur, (j + 1) / SPG, kc); // next step starts a new group
                 }
@@ -378,19 +436,18 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                 for (int q = 0; q < 4 * kRB; ++q) {
                     const int i = q / 4, t = q % 4;
                     __builtin_amdgcn_sched_barrier(0);
-                    mfma_acc<BF>(acc[i][t], bop[t], af[i % kRing]);
+                    if (q == 0 || q == 2 * kRB) lds_wait();
+                    mfma_acc<BF>(acc[i][t], bop[t], af[i]);
                     if (q == 0) load_atom(step + 4, ring[j]);
-                    if (q % 4 == 2 && q < 16) dma_a(step + 3, (j + 3) % kABufs, q / 4);
-                    if (t == 0 && i + kLead < kRB) af[(i + kLead) % kRing] = read_a(buf, i + kLead);
-                    if (t == 0 && i + kLead >= kRB)
-                        af[i + kLead - kRB] = read_a((j + 1) % kABufs, i + kLead - kRB);
-                    if (q >= kDqFirstSlot) {
+                    if (q < kRB / 2) af[kRB / 2 + q] = lds_read_block(a_lane[odd] + bcur, kRB / 2 + q);
+                    if (q >= 2 * kRB && q < 2 * kRB + kRB / 2)
+                        af[q - 2 * kRB] = lds_read_block(a_lane[odd ^ 1] + bnxt, q - 2 * kRB);
+                    if (q >= 16 && q < 32 && q % 4 == 0) dma_a(dpair, bdma, 4 * odd + (q - 16) / 4);
 #pragma unroll
-                        for (int o = dq_slot_begin(q, kDqTotal); o < dq_slot_begin(q + 1, kDqTotal); ++o) {
-                            const int u = o / kDqSteps, k = o % kDqSteps;
-                            dq_step_u(u, k, ring[(j + 1) % kCS], kc, st[u]);
-                            if (k == kDqSteps - 1) bnext[u] = st[u].out;
-                        }
+                    for (int o = dq_slot_begin<BF>(q, kDqTotal); o < dq_slot_end<BF>(q, kDqTotal); ++o) {
+                        const int u = o / kDqSteps, k = o % kDqSteps;
+                        dq_step_u(u, k, ring[(j + 1) % kCS], kc, st[u]);
+                        if (k == kDqSteps - 1) bnext[u] = st[u].out;
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -403,6 +460,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                 if (j == kCS - 1) barrier_after_a_loads<kMetaLoads + PANELS + 4>();
                 else barrier_after_a_loads<PANELS + 4>();
             }
+            const uint32_t bt = b0;        // the chunk's three buffers rotate
+            b0 = b2;
+            b2 = b1;
+            b1 = bt;
         }
         mfma_hazard_gap();
         __builtin_amdgcn_s_waitcnt(0);   // direct loads issued for steps past the segment have landed
