@@ -220,24 +220,25 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
     struct Consts {
         DqConst<BF> q[4];
     };
+    // constants of lane column u (panel u / T, column t = u % T)
+    auto make_const = [&](const Meta& mt, int m, Consts& k, int u) {
+        const int pp = u / T, t = u % T;
+        DqConst<BF>& kq = k.q[u];
+        if constexpr (BF) {
+            const uint32_t sw = mt.s[m][pp][t / 2];
+            kq.s = __builtin_bit_cast(float, (t & 1) ? (sw & 0xFFFF0000u) : (sw << 16));
+            kq.nzs = -(byte_f32(mt.z[m][pp], t) * kq.s);
+        } else {
+            const uint32_t sh = mt.s[m][pp][t / 2] >> (16 * (t & 1));
+            kq.s2 = as_h2(__builtin_amdgcn_perm(sh, sh, 0x01000100u));
+            const uint32_t n = __builtin_amdgcn_perm(0xE4E4E4E4u, mt.z[m][pp], 0x04000400u | (t * 0x00010001u));
+            kq.nz = n;
+            kq.nz64 = neg_zero64_pair(n);
+        }
+    };
     auto make_consts = [&](const Meta& mt, int m, Consts& k) {
 #pragma unroll
-        for (int pp = 0; pp < PANELS; ++pp)
-#pragma unroll
-            for (int t = 0; t < T; ++t) {
-                DqConst<BF>& kq = k.q[pp * T + t];
-                if constexpr (BF) {
-                    const uint32_t sw = mt.s[m][pp][t / 2];
-                    kq.s = __builtin_bit_cast(float, (t & 1) ? (sw & 0xFFFF0000u) : (sw << 16));
-                    kq.nzs = -(byte_f32(mt.z[m][pp], t) * kq.s);
-                } else {
-                    const uint32_t sh = mt.s[m][pp][t / 2] >> (16 * (t & 1));
-                    kq.s2 = as_h2(__builtin_amdgcn_perm(sh, sh, 0x01000100u));
-                    const uint32_t n = __builtin_amdgcn_perm(0xE4E4E4E4u, mt.z[m][pp], 0x04000400u | (t * 0x00010001u));
-                    kq.nz = n;
-                    kq.nz64 = neg_zero64_pair(n);
-                }
-            }
+        for (int u = 0; u < 4; ++u) make_const(mt, m, k, u);
     };
     // Dequantization micro-step k of B operand u (0..3) from ring slot `slot`.
     auto dq_step_u = [&](int u, int k, const u32x4 (&slot)[PANELS], const Consts& kk, DqSt<BF>& st) {
@@ -398,19 +399,24 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         // One K step s (j = s mod 4), as 64 MFMA slots (row block i = slot / 4,
         // column block t = slot % 4), each followed by at most one other
         // instruction group, fixed by scheduling fences:
-        //   slot 0        wait for this step's blocks 0..7 (read half a step
-        //                 ago); loads of the atoms for step s+4 (into the ring
-        //                 slot of step s, whose operands were formed during s-1)
+        //   slot 0        wait for this step's blocks 0..7 (read half a step ago)
         //   slots 0..7    A fragments of blocks 8..15 of step s
         //   slot 32       wait for them
         //   slots 32..39  A fragments of blocks 0..7 of step s+1
-        //   slots 16+4r   direct load r (0..3) of half of the A pair two ahead
+        //   fp16: slot 9 the atom loads for step s+4 (into the ring slot of
+        //   step s, whose operands were formed during s-1); slots 8..14 the
+        //   constants of a new group; slot 40 the metadata reload; slots
+        //   41+2r direct load r (0..3) of half of the A pair two ahead.
+        //   bf16: slot 0 the atoms, slots 16+4r the direct loads.
         //   [W, 32), [W + 32, 64)
         //                 the dequantization micro-steps of step s+1's B
         //                 operands, one vector instruction each, issued while
         //                 the matrix core works and no LDS data returns
         // then one barrier, after this wave's loads issued during step s-1
         // (the direct loads of the pair the next step may read) have landed.
+        // slots of the atom load and of the four direct loads
+        constexpr int kAtomSlot = BF ? 0 : 9;
+        constexpr int kDmaSlot = BF ? 16 : 41, kDmaStride = BF ? 4 : 2;
         for (int ch = c0; ch < c1; ++ch) {
 #pragma unroll
             for (int j = 0; j < kCS; ++j) {
@@ -420,15 +426,24 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                 const uint32_t bnxt = j == 0 ? b0 : (j == 3 ? b2 : b1);   // step s+1's pair
                 const uint32_t bdma = j < 2 ? b2 : b0;                    // pair 2 ch + 2 + j / 2
                 const int dpair = 2 * ch + 2 + (j >> 1);
-                if (j == kCS - 1) {
-                    // constants of the next chunk's first group, from metadata
-                    // that landed a chunk ago, formed before its registers
-                    // are reloaded (a load into live registers would wait)
-                    make_consts(mnext, 0, kc);
-                    if constexpr (MPC > 1) mcur = mnext;
-                    load_meta(ch + 2, mnext);
-                } else if ((j + 1) % SPG == 0) {
-                    make_consts(mcur, (j + 1) / SPG, kc); // next step starts a new group
+                // The next step starts a new metadata group (the next chunk's
+                // first, from metadata that landed a chunk ago, or the next
+                // group of this chunk): its constants are formed before this
+                // step's dequantization window, and the chunk's last step
+                // reloads the metadata registers after they are consumed (a
+                // load into registers still to be copied would have to wait).
+                // fp16 spreads this work over the quiet slots 8..15 and 40
+                // (no LDS returns, no dequantization); bf16, whose window
+                // starts at slot 8, does it before the step.
+                const bool new_group = j == kCS - 1 || (j + 1) % SPG == 0;
+                const Meta& msrc = j == kCS - 1 ? mnext : mcur;
+                const int mgrp = j == kCS - 1 ? 0 : (j + 1) / SPG;
+                if constexpr (BF) {
+                    if (new_group) make_consts(msrc, mgrp, kc);
+                    if (j == kCS - 1) {
+                        if constexpr (MPC > 1) mcur = mnext;
+                        load_meta(ch + 2, mnext);
+                    }
                 }
                 u32x4 bnext[4];
                 DqSt<BF> st[4];
@@ -438,11 +453,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                     __builtin_amdgcn_sched_barrier(0);
                     if (q == 0 || q == 2 * kRB) lds_wait();
                     mfma_acc<BF>(acc[i][t], bop[t], af[i]);
-                    if (q == 0) load_atom(step + 4, ring[j]);
+                    if (q == kAtomSlot) load_atom(step + 4, ring[j]);
+                    if constexpr (!BF) {
+                        if (new_group && q >= 8 && q < 16 && q % 2 == 0) make_const(msrc, mgrp, kc, (q - 8) / 2);
+                        if (j == kCS - 1 && q == 15) {
+                            if constexpr (MPC > 1) mcur = mnext;
+                        }
+                        if (j == kCS - 1 && q == 40) load_meta(ch + 2, mnext);
+                    }
                     if (q < kRB / 2) af[kRB / 2 + q] = lds_read_block(a_lane[odd] + bcur, kRB / 2 + q);
                     if (q >= 2 * kRB && q < 2 * kRB + kRB / 2)
                         af[q - 2 * kRB] = lds_read_block(a_lane[odd ^ 1] + bnxt, q - 2 * kRB);
-                    if (q >= 16 && q < 32 && q % 4 == 0) dma_a(dpair, bdma, 4 * odd + (q - 16) / 4);
+                    if (q >= kDmaSlot && q < kDmaSlot + 4 * kDmaStride && (q - kDmaSlot) % kDmaStride == 0)
+                        dma_a(dpair, bdma, 4 * odd + (q - kDmaSlot) / kDmaStride);
 #pragma unroll
                     for (int o = dq_slot_begin<BF>(q, kDqTotal); o < dq_slot_end<BF>(q, kDqTotal); ++o) {
                         const int u = o / kDqSteps, k = o % kDqSteps;
