@@ -118,6 +118,11 @@ __device__ __forceinline__ void mfma_hazard_gap() {
 // more later: a weight atom three steps on, metadata four.  LDS reads
 // issued before the barrier stay in flight (no LDS wait).  s_waitcnt fields:
 // vmcnt = NOW (bits 3..0 and 15..14), expcnt and lgkmcnt at their maximum.
+__device__ __forceinline__ void barrier_only() {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
 template <int NOW>
 __device__ __forceinline__ void barrier_after_a_loads() {
     static_assert(NOW >= 4 && NOW < 64, "vmcnt holds 6 bits");
@@ -403,20 +408,21 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
         //   slots 0..7    A fragments of blocks 8..15 of step s
         //   slot 32       wait for them
         //   slots 32..39  A fragments of blocks 0..7 of step s+1
-        //   fp16: slot 9 the atom loads for step s+4 (into the ring slot of
-        //   step s, whose operands were formed during s-1); slots 8..14 the
-        //   constants of a new group; slot 40 the metadata reload; slots
-        //   41+2r direct load r (0..3) of half of the A pair two ahead.
+        //   fp16: slots 8+2r direct load r (0..3) of half of the A pair two
+        //   ahead; slots 9..15 the constants of a new group; slot 41 the atom
+        //   loads for step s+4 (into the ring slot of step s, whose operands
+        //   were formed during s-1); slot 43 the metadata reload.
         //   bf16: slot 0 the atoms, slots 16+4r the direct loads.
         //   [W, 32), [W + 32, 64)
         //                 the dequantization micro-steps of step s+1's B
         //                 operands, one vector instruction each, issued while
         //                 the matrix core works and no LDS data returns
-        // then one barrier, after this wave's loads issued during step s-1
-        // (the direct loads of the pair the next step may read) have landed.
-        // slots of the atom load and of the four direct loads
-        constexpr int kAtomSlot = BF ? 0 : 9;
-        constexpr int kDmaSlot = BF ? 16 : 41, kDmaStride = BF ? 4 : 2;
+        // then one barrier (after even steps, once the direct loads of the
+        // pair about to be read ahead have landed).
+        // slots of the atom load, the metadata reload (fp16) and the four
+        // direct loads
+        constexpr int kAtomSlot = BF ? 0 : 41, kMetaSlot = 43;
+        constexpr int kDmaSlot = BF ? 16 : 8, kDmaStride = BF ? 4 : 2;
         for (int ch = c0; ch < c1; ++ch) {
 #pragma unroll
             for (int j = 0; j < kCS; ++j) {
@@ -455,11 +461,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                     mfma_acc<BF>(acc[i][t], bop[t], af[i]);
                     if (q == kAtomSlot) load_atom(step + 4, ring[j]);
                     if constexpr (!BF) {
-                        if (new_group && q >= 8 && q < 16 && q % 2 == 0) make_const(msrc, mgrp, kc, (q - 8) / 2);
-                        if (j == kCS - 1 && q == 15) {
+                        if (new_group && q >= 9 && q < 16 && q % 2 == 1) make_const(msrc, mgrp, kc, (q - 9) / 2);
+                        if (j == kCS - 1 && q == 40) {
                             if constexpr (MPC > 1) mcur = mnext;
                         }
-                        if (j == kCS - 1 && q == 40) load_meta(ch + 2, mnext);
+                        if (j == kCS - 1 && q == kMetaSlot) load_meta(ch + 2, mnext);
                     }
                     if (q < kRB / 2) af[kRB / 2 + q] = lds_read_block(a_lane[odd] + bcur, kRB / 2 + q);
                     if (q >= 2 * kRB && q < 2 * kRB + kRB / 2)
@@ -476,12 +482,27 @@ __global__ __launch_bounds__(kThreads, 1) void gemm256_kernel(
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int t = 0; t < 4; ++t) bop[t] = bnext[t];
-                // vector-memory operations of this step: metadata (last step
-                // of a chunk: two loads per group and panel), one atom load
-                // per panel, four direct loads
+                // The direct loads of a pair must have landed before the step
+                // whose next-step reads take its first fragments: pair 2 ch + 1
+                // (loaded during the previous chunk's last two steps) before
+                // step j = 1 reads ahead, pair 2 ch + 2 (loaded during j = 0,
+                // 1) before j = 3 does.  So only the even steps end with a
+                // wait, for every load but those issued after the previous
+                // step's direct loads (loads complete in order): fp16 issues
+                // its atoms (one load per panel) and metadata (two per group
+                // and panel, chunk's last step) after its direct loads, so a
+                // slow weight fetch holds up the wait one step later than
+                // it would otherwise; bf16 issues them before.  The odd
+                // steps' barrier only orders the reuse of a buffer.
                 constexpr int kMetaLoads = 2 * MPC * PANELS;
-                if (j == kCS - 1) barrier_after_a_loads<kMetaLoads + PANELS + 4>();
-                else barrier_after_a_loads<PANELS + 4>();
+                if (j % 2 == 1) {
+                    barrier_only();
+                } else if constexpr (BF) {
+                    barrier_after_a_loads<PANELS + 4>();
+                } else {
+                    if (j == 0) barrier_after_a_loads<PANELS + kMetaLoads + 4 + PANELS>();
+                    else barrier_after_a_loads<PANELS + 4 + PANELS>();
+                }
             }
             const uint32_t bt = b0;        // the chunk's three buffers rotate
             b0 = b2;
