@@ -505,18 +505,26 @@ int launch_bits(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t*
 
 }  // namespace
 
-// From M = 1024 rows up the 256 x 256 kernel runs when its tiles fill the
+// The 256 x 256 kernel runs, for the sizes below, when its tiles fill the
 // device or a workspace lets it split K (it is then the only GEMM that uses
-// a workspace); below that its 256-row tiles leave too little parallelism.
-constexpr int64_t kGemm256MinM = 1024;
+// a workspace).
+// The 256-row GEMM from M = 1024 on, and from M = 256 where K is long: its
+// stream-K split measured 12% and 29% faster than the 128-row split-K at
+// M = 512 and 768 (K = 14336, N = 4096) and equal at M = 256, while at
+// K = 4096 the 128-row kernel stays ahead below M = 1024 (M = 512 and 768 at
+// N = 14336 by 15% and 5%; W8 M = 512, K = N = 4096 by 13%).
+constexpr int64_t kGemm256MinM = 1024, kGemm256MinMLongK = 256, kLongK = 8192;
+static bool gemm256_size(const Layout& L, int64_t M) {
+    return gemm256_supported(L) && (M >= kGemm256MinM || (M >= kGemm256MinMLongK && L.K >= kLongK));
+}
 static bool use_gemm256(const Layout& L, int64_t M, const void* ws, hipStream_t s) {
-    return M >= kGemm256MinM && gemm256_supported(L) && (ws != nullptr || gemm256_fills_device(L, M, s));
+    return gemm256_size(L, M) && (ws != nullptr || gemm256_fills_device(L, M, s));
 }
 
 // Workspace either GEMM may use for this problem: the 256-row kernel's
-// stream-K (M >= 1024), else the 128-row kernel's split-K.
+// stream-K (gemm256_size), else the 128-row kernel's split-K.
 int64_t gemm_workspace_bytes(const Layout& L, int64_t M) {
-    if (M >= kGemm256MinM && gemm256_supported(L)) return gemm256_workspace_bytes(L, M);
+    if (gemm256_size(L, M)) return gemm256_workspace_bytes(L, M);
     if (!main_kernel_fits(L, L.bits)) return 0;
     const SplitPlan sp = L.bits == 4 ? plan_split<4>(L, M) : plan_split<8>(L, M);
     return split_workspace_bytes(L, M, sp);
