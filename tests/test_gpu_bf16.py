@@ -182,6 +182,7 @@ GEMM_CASES = [
     (4, 777, 4096, 2056, 128), (4, 130, 480, 264, 96),                 # 128-row GEMM, generic kernel
     (4, 1024, 1024, 2048, 128), (4, 2048, 2048, 4096, 128), (4, 1100, 1024, 1000, 128),
     (4, 4096, 1024, 4096, 128),                                        # 256-row GEMM
+    (4, 300, 8192, 520, 128), (8, 600, 8192, 264, 64),                 # 256-row GEMM, 256 <= M < 1024, long K
     (8, 1, 1024, 1024, 128), (8, 8, 2048, 520, 128), (8, 33, 1024, 1024, 64),
     (8, 512, 4096, 4096, 128), (8, 129, 1024, 264, 32), (8, 1024, 1024, 4096, 128),
     (8, 2048, 2048, 2048, 64),

@@ -183,7 +183,9 @@ GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 2
                (4, 6, 288, 72, 96), (4, 3, 256, 64, 128),
                # 17..64 rows: two or four row blocks of the streaming form
                (4, 24, 1024, 520, 128), (8, 31, 512, 72, 64), (4, 48, 2048, 264, 32), (8, 64, 1024, 2056, 128),
-               (4, 40, 768, 136, 256)]
+               (4, 40, 768, 136, 256),
+               # 256..1023 rows with K >= 8192: the 256-row kernel (stream-K), partial row tiles
+               (4, 300, 8192, 520, 128), (8, 600, 8192, 264, 64), (4, 257, 16384, 136, 32)]
 
 
 @pytest.mark.parametrize("bits,M,K,N,G", GEMM_SHAPES)
@@ -197,7 +199,7 @@ def test_gemm_parity_small(tf, bits, M, K, N, G):
                                              ("gemv", 4, 1, 32768, 64), ("gemm", 4, 1030, 8192, 512),
                                              ("gemm", 8, 1024, 4096, 768), ("gemm", 4, 16, 4096, 1024),
                                              ("gemm", 8, 5, 8192, 512), ("gemm", 4, 64, 4096, 1024),
-                                             ("gemm", 8, 33, 4096, 520)])
+                                             ("gemm", 8, 33, 4096, 520), ("gemm", 4, 300, 8192, 520)])
 def test_integer_invariant_bitexact(tf, kind, bits, M, K, N):
     """s = 1, z = 0, integer x in [-3, 3]: every partial sum is an integer below
     2^24, so the fp16 output must be RNE of the exact integer matmul."""
