@@ -43,6 +43,7 @@ EXTRA = {
     # the 256-row GEMM's K step is a fully unrolled 64-slot schedule; let the
     # unroller expand it however large the kernel around it grows
     "tf_gemm256.hip": [*_NO_LDS_PROMOTE, "-mllvm", "-pragma-unroll-threshold=1000000"],
+    "tf_gemm_ks.hip": [*_NO_LDS_PROMOTE, "-mllvm", "-pragma-unroll-threshold=1000000"],
 }
 
 

@@ -523,8 +523,25 @@ static bool use_gemm256(const Layout& L, int64_t M, const void* ws, hipStream_t 
 
 // Workspace either GEMM may use for this problem: the 256-row kernel's
 // stream-K (gemm256_size), else the 128-row kernel's split-K.
+// The 64 x 128 GEMM with K split over each workgroup's waves, where its tiles
+// (one workgroup per compute unit, no partial sums in a workspace) beat the
+// 128-row GEMM's split-K.  Measured on MI355X (graph replay, fp16, M = 65 ..
+// 1000 at K = 1024 .. 14336): 4-bit from 192 tiles, or below that while
+// K <= 4096 (one workgroup's K run stays short), up to 512 tiles (two rounds
+// of workgroups; 0.51 - 0.96 of the 128-row time; three or more rounds lose,
+// as does K = 14336 with 64 - 96 tiles); 8-bit with 192 - 256 tiles (0.79 -
+// 0.90; with fewer tiles, or a second round, the 128-row split-K is faster).
+constexpr int64_t kKsMinTiles = 192, kKsMaxTilesW4 = 512, kKsMaxTilesW8 = 256, kKsShortK = 4096;
+static bool use_gemm_ks(const Layout& L, int64_t M) {
+    if (gemm256_size(L, M) || !gemm_ks_supported(L)) return false;
+    const int64_t tiles = ((M + 63) / 64) * ((L.N + 127) / 128);
+    if (L.bits == 4) return tiles <= kKsMaxTilesW4 && (tiles >= kKsMinTiles || L.K <= kKsShortK);
+    return tiles >= kKsMinTiles && tiles <= kKsMaxTilesW8;
+}
+
 int64_t gemm_workspace_bytes(const Layout& L, int64_t M) {
     if (gemm256_size(L, M)) return gemm256_workspace_bytes(L, M);
+    if (use_gemm_ks(L, M)) return 0;
     if (!main_kernel_fits(L, L.bits)) return 0;
     const SplitPlan sp = L.bits == 4 ? plan_split<4>(L, M) : plan_split<8>(L, M);
     return split_workspace_bytes(L, M, sp);
@@ -534,6 +551,7 @@ int launch_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t
                 void* ws, size_t ws_bytes, hipStream_t s, bool bf) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
     if (use_gemm256(L, M, ws, s)) return launch_gemm256(L, A, pk, C, M, ws, ws_bytes, s, bf);
+    if (use_gemm_ks(L, M)) return launch_gemm_ks(L, A, pk, C, M, s, bf);
     // a workspace too small for this kernel's split (sized for another
     // kernel of a larger M) selects the single-pass form
     if (ws && (int64_t)ws_bytes < gemm_workspace_bytes(L, M)) ws = nullptr;

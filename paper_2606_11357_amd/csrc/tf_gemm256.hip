@@ -80,33 +80,16 @@ __device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff,
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
 
-// acc += a x b on the matrix core with the accumulator pinned to one AGPR
-// quad for the whole loop (source C and destination are the same registers).
-// Written as an asm statement because the register allocator otherwise
-// moves the 256 loop-carried accumulators between AGPRs and VGPRs at every
-// step; the asm is not volatile, so it still schedules freely.
-template <bool BF>
-__device__ __forceinline__ void mfma_acc(float4_t& acc, const u32x4& a, const u32x4& b) {
-    if constexpr (BF)
-        asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-    else
-        asm("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
 // The weights go in as the first operand and the activations as the second,
 // so each accumulator block is a 16 (n) x 16 (m) tile of C transposed: lane l
 // holds row m = l % 16 of C and four consecutive columns n = 4 (l / 16) + r,
 // which the epilogue stores as one 8-byte write.
-// The compiler does not see the MFMAs inside the asm statements, so it does
-// not insert the wait states the ISA requires between a matrix instruction
-// writing its accumulator and another instruction reading it (nor between
-// the accumulator initialisation and the first MFMA).  The loop body is its
-// own basic block, so a gap of 32 wait states placed before and after the loop
-// covers both transitions; inside the loop, accumulators are only read by
-// further MFMAs of the same shape (no wait needed) and B operands are produced
-// a whole K step (and a barrier) ahead of their use.
-__device__ __forceinline__ void mfma_hazard_gap() {
-    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7");
-}
+// Hazards around mfma_acc (see there): the loop body is its own basic block,
+// so mfma_hazard_gap() placed before and after the loop covers the
+// accumulator initialisation and the epilogue's reads; inside the loop,
+// accumulators are only read by further MFMAs of the same shape (no wait
+// needed) and B operands are produced a whole K step (and a barrier) ahead of
+// their use.
 
 // End-of-step barrier.  The A tile of step s + 3 reaches LDS by direct
 // global-to-LDS loads issued during step s; its first fragments are read

@@ -368,6 +368,28 @@ __device__ __forceinline__ float4_t mfma16(const u32x4& a, const u32x4& b, const
                                                       __builtin_bit_cast(half8_t, b), c, 0, 0, 0);
 }
 
+// acc += a x b on the matrix core with the accumulator pinned to one AGPR
+// quad (source C and destination the same registers).  An asm statement
+// because, with hundreds of loop-carried accumulators, the register
+// allocator otherwise copies them between AGPRs and VGPRs at every step; not
+// volatile, so it still schedules freely.  The compiler does not see the
+// matrix instruction inside, so it inserts none of the wait states the ISA
+// requires around it: a caller keeps at least two wait states between a
+// vector-ALU write of an operand and the MFMA that reads it, and puts
+// mfma_hazard_gap() between the accumulators' initialisation and the first
+// MFMA and between the last MFMA and the first read of the accumulators.
+template <bool BF>
+__device__ __forceinline__ void mfma_acc(float4_t& acc, const u32x4& a, const u32x4& b) {
+    if constexpr (BF)
+        asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+    else
+        asm("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// 32 wait states, more than any matrix-instruction dependency requires.
+__device__ __forceinline__ void mfma_hazard_gap() {
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7");
+}
+
 // bfloat16 pattern 0x4300 | v is exactly 128 + v for 0 <= v < 128: a nibble
 // in bits 0..3 of each half of x reads as (128 + q, 128 + q').
 constexpr uint32_t kMagicBf2 = 0x43004300u;
@@ -531,6 +553,10 @@ bool gemm256_fills_device(const Layout& L, int64_t M, hipStream_t s);
 int64_t gemm256_workspace_bytes(const Layout& L, int64_t M);
 int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
                    void* ws, size_t ws_bytes, hipStream_t s, bool bf);
+// The 64 x 128 GEMM with K split over the workgroup's waves (no workspace).
+bool gemm_ks_supported(const Layout& L);
+int launch_gemm_ks(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
+                   hipStream_t s, bool bf);
 int launch_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, size_t ws_bytes, hipStream_t s, bool bf);
 int launch_silu_mul(const uint16_t* gu, int64_t M, int64_t N, uint16_t* h, hipStream_t s, bool bf);

@@ -179,13 +179,15 @@ GEMM_CASES = [
     (4, 4, 2048, 520, 128), (4, 16, 1024, 1024, 64), (4, 17, 1024, 1032, 128),
     (4, 33, 4096, 264, 128), (4, 64, 1024, 1024, 32),                  # streaming matrix-core form
     (4, 65, 1024, 1032, 128), (4, 300, 2048, 1024, 64), (4, 200, 1024, 1024, 32),
-    (4, 777, 4096, 2056, 128), (4, 130, 480, 264, 96),                 # 128-row GEMM, generic kernel
+    (4, 777, 4096, 2056, 128),                                         # 64 x 128 GEMM, K over the waves
+    (4, 200, 8192, 264, 128), (4, 130, 480, 264, 96),                  # 128-row GEMM, generic kernel
     (4, 1024, 1024, 2048, 128), (4, 2048, 2048, 4096, 128), (4, 1100, 1024, 1000, 128),
     (4, 4096, 1024, 4096, 128),                                        # 256-row GEMM
     (4, 300, 8192, 520, 128), (8, 600, 8192, 264, 64),                 # 256-row GEMM, 256 <= M < 1024, long K
     (8, 1, 1024, 1024, 128), (8, 8, 2048, 520, 128), (8, 33, 1024, 1024, 64),
     (8, 512, 4096, 4096, 128), (8, 129, 1024, 264, 32), (8, 1024, 1024, 4096, 128),
     (8, 2048, 2048, 2048, 64),
+    (8, 384, 1152, 4088, 64), (8, 420, 640, 3968, 32),                 # 64 x 128 GEMM, 8-bit, ragged N / M
 ]
 
 

@@ -52,7 +52,7 @@ def test_tf_log_names_each_plan():
     assert "gemm256_kernel<4,1,f16> M=2048 K=4096 N=14336" in lines[0]
     assert "gemm256_kernel<4,1,f16> M=2048 K=14336 N=4096" in lines[1]
     assert "stream-K" in lines[1]
-    assert "gemm_kernel<8," in lines[2] and "M=512" in lines[2]
+    assert "gemm_ks_kernel<8," in lines[2] and "M=512" in lines[2]
     assert "gemv_kernel<4,1," in lines[3] and "vector form" in lines[3]
     assert "gemv_kernel<4,16," in lines[4] and "matrix-core form" in lines[4]
 

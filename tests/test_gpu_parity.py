@@ -185,7 +185,13 @@ GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 2
                (4, 24, 1024, 520, 128), (8, 31, 512, 72, 64), (4, 48, 2048, 264, 32), (8, 64, 1024, 2056, 128),
                (4, 40, 768, 136, 256),
                # 256..1023 rows with K >= 8192: the 256-row kernel (stream-K), partial row tiles
-               (4, 300, 8192, 520, 128), (8, 600, 8192, 264, 64), (4, 257, 16384, 136, 32)]
+               (4, 300, 8192, 520, 128), (8, 600, 8192, 264, 64), (4, 257, 16384, 136, 32),
+               # the 64 x 128 kernel with K split over the workgroup's waves: 8-bit with
+               # 192..256 tiles (ragged N with a clamped last panel; 9 and 5 chunks split
+               # unevenly over the four waves; groups of 64 and 32), 4-bit with 65 rows
+               (8, 384, 1152, 4088, 64), (8, 420, 640, 3968, 32), (4, 65, 4096, 776, 128),
+               # 4-bit beyond the 64 x 128 kernel's 512 tiles: the 128-row GEMM
+               (4, 700, 1024, 6000, 128)]
 
 
 @pytest.mark.parametrize("bits,M,K,N,G", GEMM_SHAPES)
@@ -199,7 +205,8 @@ def test_gemm_parity_small(tf, bits, M, K, N, G):
                                              ("gemv", 4, 1, 32768, 64), ("gemm", 4, 1030, 8192, 512),
                                              ("gemm", 8, 1024, 4096, 768), ("gemm", 4, 16, 4096, 1024),
                                              ("gemm", 8, 5, 8192, 512), ("gemm", 4, 64, 4096, 1024),
-                                             ("gemm", 8, 33, 4096, 520), ("gemm", 4, 300, 8192, 520)])
+                                             ("gemm", 8, 33, 4096, 520), ("gemm", 4, 300, 8192, 520),
+                                             ("gemm", 8, 384, 512, 4096), ("gemm", 4, 200, 1024, 520)])
 def test_integer_invariant_bitexact(tf, kind, bits, M, K, N):
     """s = 1, z = 0, integer x in [-3, 3]: every partial sum is an integer below
     2^24, so the fp16 output must be RNE of the exact integer matmul."""
@@ -278,12 +285,13 @@ def test_workspace_shared_across_shapes(tf):
                                            (4, 12, 16384, 512, 128), (8, 16, 14336, 1024, 128),
                                            (4, 1300, 2048, 1000, 128), (8, 1520, 1024, 776, 64),
                                            (4, 2048, 1024, 4096, 32), (4, 1100, 3072, 2320, 128),
-                                           # 128-row tiles split along K (few tiles)
-                                           (8, 512, 4096, 4096, 128), (4, 100, 4096, 3000, 128),
-                                           (4, 300, 2048, 520, 64), (8, 40, 8192, 264, 32),
-                                           (4, 700, 1536, 1000, 128), (4, 64, 8192, 1024, 128),
+                                           # 128-row tiles split along K (few tiles, long K or 8-bit)
+                                           (8, 256, 4096, 4096, 128), (4, 200, 8192, 1024, 128),
+                                           (8, 40, 8192, 264, 32), (4, 64, 8192, 1024, 128),
                                            (8, 40, 4096, 4096, 128),
-                                           # 8 and 7 K slices (12 and 37 tiles of 128 x 256)
+                                           # 64 x 128 tiles with K over the waves (no workspace either way)
+                                           (8, 512, 4096, 4096, 128), (4, 100, 4096, 3000, 128),
+                                           (4, 300, 2048, 520, 64), (4, 700, 1536, 1000, 128),
                                            (4, 100, 4096, 9400, 128)])
 def test_gemm_workspace_modes(tf, bits, M, K, N, G):
     """The K-split kernels (workspace: stream-K for 256-row tiles, split-K for
@@ -403,8 +411,9 @@ def test_gemm_hybrid_one_chunk_per_block(tf):
 def test_gemm_w4_msweep_sampled(tf, M, K, N):
     """Points of the paper's prompt-length sweep (M = 256..8192 step 256, both
     Llama-3-8B MLP shapes) at full size: sampled rows x columns against the
-    oracle, all of C finite.  Covers the 128-row split-K kernel (M = 256), the
-    256-row kernel in whole-tile and stream-K forms and the largest M."""
+    oracle, all of C finite.  Covers the 64 x 128 kernel with K split over the
+    workgroup's waves (M = 256, K = 4096), the 256-row kernel in whole-tile and
+    stream-K forms and the largest M."""
     d = make_inputs(4, M, K, N, seed=M)
     got = run(tf, "gemm", d, pack(tf, d))
     assert np.all(np.isfinite(got.astype(np.float64)))
