@@ -523,20 +523,19 @@ static bool use_gemm256(const Layout& L, int64_t M, const void* ws, hipStream_t 
 
 // Workspace either GEMM may use for this problem: the 256-row kernel's
 // stream-K (gemm256_size), else the 128-row kernel's split-K.
-// The 64 x 128 GEMM with K split over each workgroup's waves, where its tiles
-// (one workgroup per compute unit, no partial sums in a workspace) beat the
-// 128-row GEMM's split-K.  Measured on MI355X (graph replay, fp16, M = 65 ..
-// 1000 at K = 1024 .. 14336): 4-bit from 192 tiles, or below that while
-// K <= 4096 (one workgroup's K run stays short), up to 512 tiles (two rounds
-// of workgroups; 0.51 - 0.96 of the 128-row time; three or more rounds lose,
-// as does K = 14336 with 64 - 96 tiles); 8-bit with 192 - 256 tiles (0.79 -
-// 0.90; with fewer tiles, or a second round, the 128-row split-K is faster).
-constexpr int64_t kKsMinTiles = 192, kKsMaxTilesW4 = 512, kKsMaxTilesW8 = 256, kKsShortK = 4096;
+// The 64 x 128 GEMM with K split over each workgroup's waves (one workgroup
+// per compute unit, no partial sums in a workspace) wherever it beats the
+// 128-row GEMM.  Measured on MI355X (graph replay, fp16, M = 65 .. 1000 at
+// K = 1024 .. 14336, both widths): it wins up to 1120 tiles (0.43 - 0.92 of
+// the 128-row time; 896 tiles ties) and loses from 1344 (1.09 - 1.18); with
+// long K on few tiles (K = 14336, N = 4096: 64 - 96 tiles) one workgroup's
+// run of K is too long against the 128-row split-K (1.08 - 1.18), while
+// K = 8192 on 256 tiles still wins (0.75).
+constexpr int64_t kKsMaxTiles = 1200, kKsMinTilesLongK = 192, kKsLongK = 8192;
 static bool use_gemm_ks(const Layout& L, int64_t M) {
     if (gemm256_size(L, M) || !gemm_ks_supported(L)) return false;
     const int64_t tiles = ((M + 63) / 64) * ((L.N + 127) / 128);
-    if (L.bits == 4) return tiles <= kKsMaxTilesW4 && (tiles >= kKsMinTiles || L.K <= kKsShortK);
-    return tiles >= kKsMinTiles && tiles <= kKsMaxTilesW8;
+    return tiles <= kKsMaxTiles && (L.K <= kKsLongK || tiles >= kKsMinTilesLongK);
 }
 
 int64_t gemm_workspace_bytes(const Layout& L, int64_t M) {

@@ -4,16 +4,20 @@
 //   C[M, N] = A[M, K] x dequant(packed)[K, N], fp16 or bf16 MFMA, fp32 sums.
 //
 // Workgroup tile 64 x 128, four waves, one per SIMD.  Each wave computes the
-// whole tile over its own quarter of K (a contiguous run of 128-row chunks)
-// and streams it alone: no LDS and no barrier inside the loop, and no
-// partial sum leaves the compute unit.
-//  - The wave's A fragments (4 row blocks of 16 rows) and the packed atoms of
-//    the tile's columns (one per panel per 32-row step) go from memory
-//    straight into a register ring of four steps, requested three steps before
-//    their use; the metadata of a group is requested with the atoms of the
-//    step that opens it.  Requests are issued metadata first, then atoms, then
-//    A, in the order the step that waits for them needs them (vector-memory
-//    loads complete in order).
+// whole tile over its own quarter of K (a contiguous run of 128-row chunks),
+// and no partial sum leaves the compute unit; inside the loop the waves share
+// nothing and never wait for each other.
+//  - A goes through a private LDS ring of four buffers per wave, each one pair
+//    of 32-row steps (64 rows x 128 bytes), requested three pairs ahead by
+//    direct global-to-LDS loads that move 8 whole rows each; the wave reads
+//    each step's MFMA fragments (16 rows x 16 bytes per lane) a step ahead.
+//    (The fragment layout straight from memory, 16 rows x 64 bytes per load,
+//    cost a fifth more time.)
+//  - The packed atoms of the tile's columns (one per panel per step) go into
+//    a register ring of four steps, requested three steps ahead; the metadata
+//    of a group travels with the atoms of the step that opens it.  All loads
+//    are asm statements with counted waits, issued metadata, atoms, A in the
+//    order their waits need them (vector-memory loads complete in order).
 //  - A step's 32 MFMAs run column block by column block (8 blocks of 16
 //    columns, each against the 4 row blocks); while the four MFMAs of block u
 //    run, the wave dequantizes (Eq. 2, rounded once, the same arithmetic as
@@ -40,17 +44,23 @@ constexpr int kKsLead = 3;              // steps between a request and its step
 constexpr int kKsRB = kKsBM / 16;       // row blocks
 constexpr int kKsNB = kKsBN / 16;       // column blocks: B operands per step
 constexpr int kKsXcds = 8;
+constexpr int kKsRing = 4;              // A buffers per wave, one pair of steps each
+constexpr int kKsPairBytes = kKsBM * 2 * kKsBK * 2;   // 64 rows x 128 bytes
+constexpr int kKsALead = 3;             // pairs between a pair's A request and its first step
 
 // A step's 32 MFMA slots, block u = slot / 4 (columns 16 u ..), row block
-// i = slot % 4.  Requests for step + 3 sit at fixed slots: the metadata (when
-// step + 3 opens a group) at kKsMetaSlot, the atoms at kKsAtomSlot, the A
-// fragment of row block r at kKsASlot + kKsASlotStride * r.
+// i = slot % 4.  Requests sit at fixed slots: the metadata of step + 3 (when
+// it opens a group) at kKsMetaSlot, its atoms at kKsAtomSlot, and the step's
+// four direct loads of A (half a pair) at kKsASlot + kKsASlotStride * r.
 constexpr int kKsMetaSlot = 0, kKsAtomSlot = 4, kKsASlot = 8, kKsASlotStride = 3;
-// The step waits twice: for its own A at block 0, for the next step's atoms
-// and metadata at block kKsMetaWaitBlock; the constants of the group the next
-// step opens are formed after that, those of block v at slot kKsConstSlot[v]
-// (block v's old constants were last used under block v - 1).
+// The step waits twice: for its own fragments (LDS reads) at block 0, for
+// the next step's atoms and metadata, and so for every pair of A requested
+// before them, at block kKsMetaWaitBlock; the next step's fragments are read
+// from kKsReadSlot, and the constants of the group the next step opens are
+// formed after that wait, those of block v at slot kKsConstSlot[v] (block v's
+// old constants were last used under block v - 1).
 constexpr int kKsMetaWaitBlock = 5;
+constexpr int kKsReadSlot = 24;         // the next step's fragments, after that wait
 constexpr int kKsConstSlot[8] = {20, 21, 22, 23, 24, 25, 26, 28};
 static_assert(kKsMetaSlot < kKsAtomSlot && kKsAtomSlot < kKsASlot, "requests go out metadata, atoms, A");
 static_assert(kKsASlot + kKsASlotStride * (kKsRB - 1) < kKsMetaWaitBlock * kKsRB,
@@ -63,6 +73,13 @@ constexpr bool ks_const_slots_ok() {
     return true;
 }
 static_assert(ks_const_slots_ok(), "constants formed after the wait and after their old value's last use");
+static_assert(kKsReadSlot >= kKsMetaWaitBlock * kKsRB && kKsReadSlot < kKsNB * kKsRB,
+              "the next step's fragments are read after the wait that completes their pair");
+// The pair holding step s + 1 was requested during steps up to
+// 2 (kKsALead - 1) before it, which the wait at step s completes when that is
+// at least 4 (everything issued up to step s - 3); a buffer is refilled only
+// after the last read of the pair it held.
+static_assert(2 * (kKsALead - 1) >= 4 && kKsRing >= kKsALead + 1, "A lead and ring size");
 
 // Buffer resource words (raw buffer, 32-bit format) for the asm loads.
 __device__ __forceinline__ i32x4 rsrc_words(const void* base, uint32_t bytes) {
@@ -111,6 +128,23 @@ __device__ __forceinline__ void vm_wait(int n) {
 // above the wait, and it stays allocated until then.
 template <typename V>
 __device__ __forceinline__ void tie(V& v) { asm volatile("" : "+v"(v)); }
+// 16 bytes per lane from a buffer straight into LDS at lds + 16 * lane (M0
+// holds the LDS address; nothing else in these kernels uses M0).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(i32x4 r, uint32_t voff, uint32_t soff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+                 :: "v"(voff), "s"(r), "s"(soff), "s"(lds) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+template <int OFF>
+__device__ __forceinline__ u32x4 ds_read16(uint32_t addr) {
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+    return v;
+}
+// Every LDS read of this wave has returned.
+__device__ __forceinline__ void lgkm_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 // MPC: metadata groups per chunk (1 when a group spans the chunk, else chunk
 // rows / group).
@@ -125,7 +159,10 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     constexpr int SPG = kKsCS / MPC;          // steps per metadata group
     constexpr int S = dq_steps<BF, BITS>();   // dequantization micro-steps per operand
     static_assert(kKsRB + 2 * (kKsRB + 3 * PANELS) <= 40, "counted waits stay within vm_wait's range");
-    __shared__ __align__(16) float4_t red[kKsWaves][kKsRB * kKsNB][64];
+    // A's per-wave rings during the loop; the K quarters' sums after it
+    // (wave w's quarter of the sum buffer is exactly its own ring)
+    __shared__ __align__(16) float4_t lds[kKsWaves][kKsRB * kKsNB][64];
+    static_assert(sizeof(lds) == kKsWaves * kKsRing * kKsPairBytes, "ring and sum buffer coincide");
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -156,18 +193,22 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     const int chunks = __builtin_amdgcn_readfirstlane(qch + (wave < rch ? 1 : 0));
     const int st0 = ch0 * kKsCS, steps = chunks * kKsCS;
 
-    // A: fragment of row block i = rows 16 i + c, halves 8 kg .. 8 kg + 7 of
-    // the step's 32; rows past M read row M - 1 (in bounds, never stored).
-    // Buffer loads: a per-lane offset fixed for the whole loop and a scalar
-    // offset per step, so no address arithmetic runs in the loop.
+    // A: the wave's K quarter in pairs of steps (64 rows x 128 bytes), each
+    // through one buffer of the wave's LDS ring.  A direct load moves 8 whole
+    // rows (lane l: row l / 8 of the 8, 16-byte chunk (l % 8) ^ (row % 8) to
+    // LDS position l % 8); rows past M read zeros (outside the buffer; never
+    // stored).  The fragment of row block i for step s (half h of its pair):
+    // lane l reads row 16 i + c at chunk 4 h + kg, held at position
+    // (4 h + kg) ^ (c % 8).
     const int rows = __builtin_amdgcn_readfirstlane(min(M - tm * kKsBM, kKsBM));
     const i32x4 ar = rsrc_words(A + row0 * K, (uint32_t)rows * (uint32_t)K * 2u);
-    uint32_t aoff[kKsRB];
+    const int pairs = steps / 2;
+    const uint32_t wlds = __builtin_amdgcn_readfirstlane(
+        (uint32_t)reinterpret_cast<uintptr_t>(&lds[0][0][0]) + (uint32_t)wave * (kKsRing * kKsPairBytes));
+    const uint32_t vb = (uint32_t)(lane >> 3) * (uint32_t)K * 2u + (uint32_t)((lane & 7) ^ (lane >> 3)) * 16u;
+    uint32_t rb[2];
 #pragma unroll
-    for (int i = 0; i < kKsRB; ++i) {
-        const uint32_t r = (uint32_t)min(16 * i + c, rows - 1);
-        aoff[i] = (r * (uint32_t)K + 8u * kg) * 2u;
-    }
+    for (int h = 0; h < 2; ++h) rb[h] = wlds + (uint32_t)(c * 128 + (((4 * h + kg) ^ (c & 7)) * 16));
     // B: atoms and metadata of the tile's panels; panels past N read the last
     // panel (in bounds, never stored).
     i32x4 wr[PANELS], sr[PANELS], zr[PANELS];
@@ -181,7 +222,6 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     const uint32_t woff = lane * 16, soff = c * T * 2, zoff = c * T;
 
     struct Slot {
-        u32x4 a[kKsRB];
         u32x4 w[PANELS];
     };
     struct Meta {
@@ -193,10 +233,22 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
 #pragma unroll
         for (int pp = 0; pp < PANELS; ++pp) sl.w[pp] = ld128(wr[pp], woff, (uint32_t)(st0 + step) * 1024u);
     };
-    auto load_a = [&](int step, int i, Slot& sl) {
-        step = min(step, steps - 1);
-        sl.a[i] = ld128(ar, aoff[i], (uint32_t)(st0 + step) * (kKsBK * 2));
+    // direct load g (0..7, rows 8 g ..) of pair `pair`'s A into its ring buffer
+    auto dma_a = [&](int pair, int g) {
+        const uint32_t buf = wlds + (uint32_t)(pair & (kKsRing - 1)) * kKsPairBytes + (uint32_t)g * 1024u;
+        pair = min(pair, pairs - 1);       // clamped: a repeated valid pair, never read
+        dma16(ar, vb, (uint32_t)(st0 + 2 * pair) * (kKsBK * 2) + (uint32_t)g * 16u * (uint32_t)K, buf);
     };
+    // the four fragments of step `step` from its pair's buffer
+    auto read_af = [&](int step, u32x4 (&af)[kKsRB]) {
+        const uint32_t base = rb[step & 1] + (uint32_t)((step >> 1) & (kKsRing - 1)) * kKsPairBytes;
+        af[0] = ds_read16<0 * 16 * 128>(base);
+        af[1] = ds_read16<1 * 16 * 128>(base);
+        af[2] = ds_read16<2 * 16 * 128>(base);
+        af[3] = ds_read16<3 * 16 * 128>(base);
+    };
+    // the direct loads issued during step t: half t % 2 of pair t / 2 + 3
+    auto dma_step = [&](int t, int r) { dma_a((t >> 1) + kKsALead, 4 * (t & 1) + r); };
     auto load_meta = [&](int step, Meta& mt) {
         step = min(step, steps - 1);
         const uint32_t g = (uint32_t)(((st0 + step) * kKsBK) >> gshift);
@@ -225,8 +277,6 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
         }
     };
     auto tie_slot = [&](Slot& sl) {
-#pragma unroll
-        for (int i = 0; i < kKsRB; ++i) tie(sl.a[i]);
 #pragma unroll
         for (int pp = 0; pp < PANELS; ++pp) tie(sl.w[pp]);
     };
@@ -259,22 +309,30 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
 #pragma unroll
         for (int u = 0; u < kKsNB; ++u) acc[i][u] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-    // Prologue: steps 0 .. 2 requested in the loop's order (metadata of the
-    // groups they open, atoms, A); constants of step 0's group; B operand of
-    // step 0, block 0.  Metadata slot m holds the group that opens at chunk
-    // step m * SPG.
+    // Prologue: the requests of steps -6 .. -1 in the loop's order (the
+    // direct loads of pairs 0 and 1 and half of 2... as steps -6 .. -4 issue
+    // them; then per step -3 .. -1 the metadata and atoms of step + 3 and its
+    // half pair), so the loop's counted waits see the same queue at its entry
+    // as at its back edge; then step 0's constants, B operand and fragments.
+    // Metadata slot m holds the group that opens at chunk step m * SPG.
     Slot ring[kKsCS];
     Meta meta[MPC];
+#pragma unroll
+    for (int t = -6; t < -3; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dma_step(t, r);
 #pragma unroll
     for (int j = 0; j < kKsLead; ++j) {
         if (j % SPG == 0) load_meta(j, meta[j / SPG]);
         load_w(j, ring[j]);
 #pragma unroll
-        for (int i = 0; i < kKsRB; ++i) load_a(j, i, ring[j]);
+        for (int r = 0; r < 4; ++r) dma_step(j - kKsLead, r);
     }
-    vm_wait(kKsRB + loads_for(1) + loads_for(2));     // step 0's metadata and atoms
+    vm_wait(4 + loads_for(1) + loads_for(2));     // step 0's metadata, atoms and pair
     tie_meta(meta[0]);
     tie_slot(ring[0]);
+    u32x4 af[2][kKsRB];
+    read_af(0, af[0]);
     DqConst<BF> kc[kKsNB];
 #pragma unroll
     for (int u = 0; u < kKsNB; ++u) kc[u] = make_const(meta[0], u);
@@ -317,17 +375,17 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
                         // first MFMA
                         asm volatile("s_nop 1");
                         if (u == 0) {
-                            // this step's A: everything requested for steps
-                            // up to this one has landed, the requests for the
-                            // next two steps stay in flight
-                            vm_wait(loads_for(j + 1) + loads_for(j + 2));
+                            // this step's fragments (read a step ago)
+                            lgkm_wait();
 #pragma unroll
-                            for (int r = 0; r < kKsRB; ++r) tie(ring[j].a[r]);
+                            for (int r = 0; r < kKsRB; ++r) tie(af[j & 1][r]);
                         }
                         if (u == kKsMetaWaitBlock) {
-                            // the next step's atoms and metadata (its A and
-                            // the requests of the last two steps in flight)
-                            vm_wait(kKsRB + loads_for(j + 2) + loads_for(j + 3));
+                            // the next step's atoms and metadata, and with
+                            // them the A pairs requested before them (the
+                            // direct loads that followed them and the
+                            // requests of the last two steps in flight)
+                            vm_wait(4 + loads_for(j + 2) + loads_for(j + 3));
 #pragma unroll
                             for (int pp = 0; pp < PANELS; ++pp) tie(ring[jn].w[pp]);
                             if (new_group) tie_meta(meta[jn / SPG]);
@@ -336,8 +394,9 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
                     }
                     if (meta_req && q == kKsMetaSlot) load_meta(step + kKsLead, meta[jl / SPG]);
                     if (q == kKsAtomSlot) load_w(step + kKsLead, ring[jl]);
-                    if (q >= kKsASlot && q < kKsASlot + kKsASlotStride * kKsRB && (q - kKsASlot) % kKsASlotStride == 0)
-                        load_a(step + kKsLead, (q - kKsASlot) / kKsASlotStride, ring[jl]);
+                    if (q >= kKsASlot && q < kKsASlot + kKsASlotStride * 4 && (q - kKsASlot) % kKsASlotStride == 0)
+                        dma_step(step, (q - kKsASlot) / kKsASlotStride);
+                    if (q == kKsReadSlot) read_af(step + 1, af[(j + 1) & 1]);
                     // constants of the group step + 1 opens; block v's old
                     // ones were last used under block v - 1
 #pragma unroll
@@ -345,7 +404,7 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
                         if (new_group && q == kKsConstSlot[v]) kc[v] = make_const(meta[jn / SPG], v);
 #pragma unroll
                     for (int k = i * S / kKsRB; k < (i + 1) * S / kKsRB; ++k) dq_micro(k, src, du, kc[du], st);
-                    mfma_acc<BF>(acc[i][u], bop[u & 1], ring[j].a[i]);
+                    mfma_acc<BF>(acc[i][u], bop[u & 1], af[j & 1][i]);
                 }
                 bop[du & 1] = st.out;
             }
@@ -355,8 +414,13 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     // the requests of the last three steps (clamped, unused) land before any
     // of their registers is reused
     vm_wait(0);
+    lgkm_wait();
 #pragma unroll
     for (int j = 0; j < kKsCS; ++j) tie_slot(ring[j]);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int r = 0; r < kKsRB; ++r) tie(af[h][r]);
 #pragma unroll
     for (int m = 0; m < MPC; ++m) tie_meta(meta[m]);
     mfma_hazard_gap();
@@ -366,16 +430,16 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
 #pragma unroll
     for (int i = 0; i < kKsRB; ++i)
 #pragma unroll
-        for (int u = 0; u < kKsNB; ++u) red[wave][i * kKsNB + u][lane] = acc[i][u];
+        for (int u = 0; u < kKsNB; ++u) lds[wave][i * kKsNB + u][lane] = acc[i][u];
     __syncthreads();
     const int i = wave;
     const int64_t row = row0 + 16 * i + c;
 #pragma unroll
     for (int u = 0; u < kKsNB; ++u) {
         const int b = i * kKsNB + u;
-        float4_t v = red[0][b][lane];
+        float4_t v = lds[0][b][lane];
 #pragma unroll
-        for (int w = 1; w < kKsWaves; ++w) v += red[w][b][lane];
+        for (int w = 1; w < kKsWaves; ++w) v += lds[w][b][lane];
         // weights were the first MFMA operand: lane holds row c of the block
         // and columns 4 kg .. 4 kg + 3 (N % 8 == 0, so all four or none fit)
         const int64_t col = col0 + 16 * u + 4 * kg;

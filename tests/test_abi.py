@@ -163,12 +163,13 @@ COUNTERS = 8 * KIB          # arrival counters at offset 0: one u32 per 32 colum
     (4, 2048, 14336, 4096, COUNTERS + 2 * 256 * 256 * 256 * 4),
     (4, 1024, 4096, 14336, COUNTERS + 2 * 256 * 256 * 256 * 4),
     (4, 2048, 4096, 16384, 0),                       # 512 tiles: whole waves, no split
-    # 128-row GEMM split-K: one 128 x 256 fp32 partial per (tile, slice), and
-    # the slices bring the work to 256 units (32 tiles x 8)
-    (8, 256, 4096, 4096, COUNTERS + 256 * 128 * 256 * 4),
-    # 64 x 128 GEMM with K split over each workgroup's waves (256 and 224
-    # tiles): the K quarters are summed in LDS, no workspace
+    # 128-row GEMM split-K (long K on few tiles): one 128 x 256 fp32 partial
+    # per (tile, slice), 16 tiles x 8 slices
+    (4, 128, 14336, 4096, COUNTERS + 16 * 8 * 128 * 256 * 4),
+    # 64 x 128 GEMM with K split over each workgroup's waves: the K quarters
+    # are summed in LDS, no workspace
     (8, 512, 4096, 4096, 0),
+    (8, 256, 4096, 4096, 0),
     (4, 128, 4096, 14336, 0),
     # decode GEMV on 64 panels of 64 columns, K split in 4 slices: one fp32
     # partial per (panel, slice, row)

@@ -118,8 +118,10 @@ def code(seq):
 
 def check_vm_waits(seq):
     """Violations of the counted waits: a use or overwrite of a VGPR whose
-    buffer load may still be in flight (loads complete in issue order)."""
-    queue, bad = [], []
+    buffer load or LDS read may still be in flight (each kind completes in
+    issue order; an LDS read counts as pending until an lgkmcnt wait leaves
+    fewer LDS reads in flight, whatever scalar loads share that counter)."""
+    queue, lgkm, bad = [], [], []
     for op, a in seq:
         args = split_args(a)
         if op == "s_waitcnt":
@@ -127,10 +129,23 @@ def check_vm_waits(seq):
             if m:
                 n = int(m.group(1))
                 queue = queue[max(0, len(queue) - n):]
+            m = re.search(r"lgkmcnt\((\d+)\)", a)
+            if m:
+                n = int(m.group(1))
+                lgkm = lgkm[max(0, len(lgkm) - n):]
             continue
-        if op.startswith("buffer_load") and not a.endswith(" lds"):
+        if op.startswith("ds_read"):
             dst = regs(args[0])
-            srcs = set().union(*[regs(x) for x in args[1:]]) if len(args) > 1 else set()
+            if any(q & (dst | regs(args[1])) for q in queue + lgkm):
+                bad.append((op, a))
+            lgkm.append(dst)
+            continue
+        if op.startswith("buffer_load"):
+            # a direct-to-LDS load counts in the same queue but targets no VGPR
+            # (its first operand is then the offset it reads)
+            to_lds = a.endswith(" lds")
+            dst = set() if to_lds else regs(args[0])
+            srcs = set().union(*[regs(x) for x in (args if to_lds else args[1:])])
             if any(q & (dst | srcs) for q in queue):
                 bad.append((op, a))
             queue.append(dst)
@@ -145,7 +160,7 @@ def check_vm_waits(seq):
         else:
             srcs = set().union(*[regs(x) for x in args]) if args else set()
             dsts = set()
-        if any(q & (srcs | dsts) for q in queue):
+        if any(q & (srcs | dsts) for q in queue + lgkm):
             bad.append((op, a))
     return bad
 
@@ -216,6 +231,14 @@ def test_checkers_catch_planted_violations():
     assert len(check_vm_waits(early)) == 1
     overwrite = [("buffer_load_dwordx4", "v[4:7], v1, s[8:11], s12 offen"), ("v_mov_b32", "v5, 0")]
     assert len(check_vm_waits(overwrite)) == 1
+    behind_lds = [("buffer_load_dwordx4", "v[4:7], v1, s[8:11], s12 offen"),
+                  ("buffer_load_dwordx4", "v2, s[8:11], s13 offen lds"), ("s_waitcnt", "vmcnt(1)"),
+                  ("v_mov_b32", "v3, v4")]            # the direct load keeps one slot: v4 is complete
+    assert check_vm_waits(behind_lds) == []
+    assert len(check_vm_waits(behind_lds[:2] + [("s_waitcnt", "vmcnt(2)"), ("v_mov_b32", "v3, v4")])) == 1
+    lds = [("ds_read_b128", "v[4:7], v1 offset:16"), ("ds_read_b128", "v[8:11], v1 offset:32")]
+    assert check_vm_waits(lds + [("s_waitcnt", "lgkmcnt(1)"), ("v_mov_b32", "v2, v4")]) == []
+    assert len(check_vm_waits(lds + [("s_waitcnt", "lgkmcnt(1)"), ("v_mov_b32", "v2, v8")])) == 1
     mf = ("v_mfma_f32_16x16x32_f16", "a[0:3], v[10:13], v[20:23], a[0:3]")
     assert len(check_mfma_hazards([("v_pk_mul_f16", "v11, v1, v2"), mf])) == 1
     assert check_mfma_hazards([("v_pk_mul_f16", "v11, v1, v2"), ("s_nop", "1"), mf]) == []

@@ -190,8 +190,9 @@ GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 2
                # 192..256 tiles (ragged N with a clamped last panel; 9 and 5 chunks split
                # unevenly over the four waves; groups of 64 and 32), 4-bit with 65 rows
                (8, 384, 1152, 4088, 64), (8, 420, 640, 3968, 32), (4, 65, 4096, 776, 128),
-               # 4-bit beyond the 64 x 128 kernel's 512 tiles: the 128-row GEMM
-               (4, 700, 1024, 6000, 128)]
+               # the 128-row GEMM: 4-bit beyond the 64 x 128 kernel's 1200 tiles, and
+               # long K on few tiles (split-K)
+               (4, 1000, 1024, 10000, 128), (4, 200, 12288, 520, 128), (8, 100, 16384, 264, 64)]
 
 
 @pytest.mark.parametrize("bits,M,K,N,G", GEMM_SHAPES)
@@ -285,10 +286,10 @@ def test_workspace_shared_across_shapes(tf):
                                            (4, 12, 16384, 512, 128), (8, 16, 14336, 1024, 128),
                                            (4, 1300, 2048, 1000, 128), (8, 1520, 1024, 776, 64),
                                            (4, 2048, 1024, 4096, 32), (4, 1100, 3072, 2320, 128),
-                                           # 128-row tiles split along K (few tiles, long K or 8-bit)
-                                           (8, 256, 4096, 4096, 128), (4, 200, 8192, 1024, 128),
+                                           # 128-row tiles split along K (few tiles, long K)
+                                           (4, 200, 12288, 1024, 128), (8, 100, 16384, 520, 64),
                                            (8, 40, 8192, 264, 32), (4, 64, 8192, 1024, 128),
-                                           (8, 40, 4096, 4096, 128),
+                                           (8, 40, 4096, 4096, 128), (8, 256, 4096, 4096, 128),
                                            # 64 x 128 tiles with K over the waves (no workspace either way)
                                            (8, 512, 4096, 4096, 128), (4, 100, 4096, 3000, 128),
                                            (4, 300, 2048, 520, 64), (4, 700, 1536, 1000, 128),
