@@ -45,6 +45,9 @@ GEMM_COPIES = 17
 # milliseconds of full load to settle, and a warm-up of a few steps (a few
 # milliseconds) leaves the first timed launches slower.
 WARM_FLOOR_S = 0.3
+# The sweeps replay each workload's graph for at least this long before
+# timing it, for the same reason.
+SWEEP_WARM_S = 0.15
 PEAK_F16_TFLOPS = 2516.6      # 256 CU x 4096 FLOP/clk x 2.4 GHz (dense fp16 or bf16 MFMA)
 PEAK_HBM_GBS = 8000.0
 COPY_BYTES = 1 << 30
@@ -246,6 +249,16 @@ def sweep(torch, tf, make_inputs, reps=50, dtypes=("f16", "bf16"), only=None):
                 torch.cuda.empty_cache()
 
 
+def warm_graph(torch, g, seconds=SWEEP_WARM_S):
+    """Replay a captured graph until `seconds` of wall time have passed."""
+    t0 = time.perf_counter()
+    while True:
+        g.replay()
+        torch.cuda.synchronize()
+        if time.perf_counter() - t0 >= seconds:
+            return
+
+
 def sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps, dtype="f16"):
     fn = getattr(tf, f"w{bits}a16_{entry}")
     ncopy = len(copies)
@@ -258,8 +271,7 @@ def sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps,
     with torch.cuda.graph(g):
         for i in range(reps):
             fn(x, copies[i % ncopy], K, N, GROUP, out=y)
-    g.replay()
-    torch.cuda.synchronize()
+    warm_graph(torch, g)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(3):
@@ -282,7 +294,8 @@ def sweep_one(torch, tf, stream, name, entry, bits, M, K, N, x, y, copies, reps,
 
 
 def graph_time_us(torch, fn, reps):
-    """Mean µs per call of fn() over 3 replays of a HIP graph of `reps` calls."""
+    """Mean µs per call of fn() over 3 replays of a HIP graph of `reps` calls
+    (after replaying it for SWEEP_WARM_S)."""
     stream = torch.cuda.current_stream()
     for _ in range(3):
         fn(0)
@@ -291,8 +304,7 @@ def graph_time_us(torch, fn, reps):
     with torch.cuda.graph(g):
         for i in range(reps):
             fn(i)
-    g.replay()
-    torch.cuda.synchronize()
+    warm_graph(torch, g)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(3):
@@ -459,8 +471,7 @@ def msweep(torch, tf, make_inputs, target_ms=6.0):
             with torch.cuda.graph(g):
                 for i in range(reps):
                     tf.w4a16_gemm(x, copies[i % ncopy], K, N, GROUP, out=y)
-            g.replay()
-            torch.cuda.synchronize()
+            warm_graph(torch, g)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             for _ in range(3):
