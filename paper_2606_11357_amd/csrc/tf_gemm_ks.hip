@@ -196,7 +196,7 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     // A: the wave's K quarter in pairs of steps (64 rows x 128 bytes), each
     // through one buffer of the wave's LDS ring.  A direct load moves 8 whole
     // rows (lane l: row l / 8 of the 8, 16-byte chunk (l % 8) ^ (row % 8) to
-    // LDS position l % 8); rows past M read zeros (outside the buffer; never
+    // LDS position l % 8); rows past M read row M - 1 (in bounds; never
     // stored).  The fragment of row block i for step s (half h of its pair):
     // lane l reads row 16 i + c at chunk 4 h + kg, held at position
     // (4 h + kg) ^ (c % 8).
@@ -205,7 +205,16 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     const int pairs = steps / 2;
     const uint32_t wlds = __builtin_amdgcn_readfirstlane(
         (uint32_t)reinterpret_cast<uintptr_t>(&lds[0][0][0]) + (uint32_t)wave * (kKsRing * kKsPairBytes));
-    const uint32_t vb = (uint32_t)(lane >> 3) * (uint32_t)K * 2u + (uint32_t)((lane & 7) ^ (lane >> 3)) * 16u;
+    // Each direct load's row offset sits in its own per-lane offset (rows past
+    // M clamped to the last row, so every read stays inside A whatever part of
+    // the address the buffer's range check covers); the pair's K offset is the
+    // scalar offset.
+    uint32_t vb[8];
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+        const uint32_t row = (uint32_t)min(8 * g + (lane >> 3), rows - 1);
+        vb[g] = row * (uint32_t)K * 2u + (uint32_t)((lane & 7) ^ (lane >> 3)) * 16u;
+    }
     uint32_t rb[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) rb[h] = wlds + (uint32_t)(c * 128 + (((4 * h + kg) ^ (c & 7)) * 16));
@@ -237,7 +246,7 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     auto dma_a = [&](int pair, int g) {
         const uint32_t buf = wlds + (uint32_t)(pair & (kKsRing - 1)) * kKsPairBytes + (uint32_t)g * 1024u;
         pair = min(pair, pairs - 1);       // clamped: a repeated valid pair, never read
-        dma16(ar, vb, (uint32_t)(st0 + 2 * pair) * (kKsBK * 2) + (uint32_t)g * 16u * (uint32_t)K, buf);
+        dma16(ar, vb[g], (uint32_t)(st0 + 2 * pair) * (kKsBK * 2), buf);
     };
     // the four fragments of step `step` from its pair's buffer
     auto read_af = [&](int step, u32x4 (&af)[kKsRB]) {
