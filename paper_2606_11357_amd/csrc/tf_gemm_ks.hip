@@ -152,7 +152,7 @@ template <int BITS, int MPC, bool BF>
 __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
     int M, int K, int N, int gshift, int64_t s_off, int64_t z_off, int na, int ng, int np,
-    int tiles_m, int tiles_n) {
+    int tiles_m, int tiles_n, KsRange rg) {
     constexpr int PW = BITS == 4 ? 64 : 32;   // columns per panel (one atom per step)
     constexpr int T = PW / 16;                // column blocks per panel
     constexpr int PANELS = kKsBN / PW;
@@ -170,10 +170,11 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     const uint32_t magic = magic_reg();
 
     // Block b runs on XCD b % 8, which takes the (b % 8)-th contiguous band
-    // of tiles; row tiles vary fastest.
+    // of the tile list: all tiles with row tiles varying fastest, or, over a
+    // range of 256 x 256 tiles, the 8 tiles of 64 x 128 of each in turn.
     int unit;
     {
-        const int total = tiles_m * tiles_n;
+        const int total = rg.count ? rg.count * 8 : tiles_m * tiles_n;
         const int b = blockIdx.x;
         const int per = total / kKsXcds, rem = total % kKsXcds;
         const int x = b % kKsXcds, i = b / kKsXcds;
@@ -182,9 +183,21 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     // (pinned to scalar registers: integer division runs on the vector ALU,
     // and buffer resources built from a value the compiler cannot prove
     // uniform would be loaded lane by lane)
-    const int tm = __builtin_amdgcn_readfirstlane(unit % tiles_m);
-    const int tn = __builtin_amdgcn_readfirstlane(unit / tiles_m);
+    int tm, tn;
+    if (rg.count) {
+        const int t = rg.tile0 + unit / 8, sub = unit % 8;
+        const int tm2 = rg.col_major ? t % rg.tiles_m : t / rg.tiles_n;
+        const int tn2 = rg.col_major ? t / rg.tiles_m : t % rg.tiles_n;
+        tm = __builtin_amdgcn_readfirstlane(4 * tm2 + sub / 2);
+        tn = __builtin_amdgcn_readfirstlane(2 * tn2 + sub % 2);
+    } else {
+        tm = __builtin_amdgcn_readfirstlane(unit % tiles_m);
+        tn = __builtin_amdgcn_readfirstlane(unit / tiles_m);
+    }
     const int64_t row0 = (int64_t)tm * kKsBM, col0 = (int64_t)tn * kKsBN;
+    // a 64 x 128 part of a 256 x 256 tile can lie wholly past C (the whole
+    // workgroup leaves before any load or barrier)
+    if (row0 >= M || col0 >= N) return;
 
     // This wave's K quarter (the launcher guarantees at least one chunk each).
     const int nch = na / kKsCS;
@@ -460,27 +473,44 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
 }
 
 template <int BITS, int MPC, bool BF>
-int launch_ks(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M, hipStream_t s) {
+int launch_ks(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M, const KsRange& rg,
+              hipStream_t s) {
     const int tiles_m = (int)((M + kKsBM - 1) / kKsBM);
     const int tiles_n = (int)((L.N + kKsBN - 1) / kKsBN);
     const int gshift = __builtin_ctz((unsigned)L.group);
-    if (log_enabled())
-        log_plan("gemm_ks_kernel<%d,%d,%s> M=%lld K=%lld N=%lld G=%d: %dx%d tiles of 64x128, K in 4 quarters "
-                 "per workgroup", BITS, MPC, BF ? "bf16" : "f16", (long long)M, (long long)L.K, (long long)L.N,
-                 L.group, tiles_m, tiles_n);
-    return launch(gemm_ks_kernel<BITS, MPC, BF>, dim3((unsigned)(tiles_m * tiles_n)), dim3(kKsThreads), 0, s, A,
-                  pk, C, (int)M, (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na, (int)L.ng, (int)L.np,
-                  tiles_m, tiles_n);
+    const int blocks = rg.count ? rg.count * 8 : tiles_m * tiles_n;
+    if (log_enabled()) {
+        if (rg.count)
+            log_plan("  gemm_ks_kernel<%d,%d,%s>: 256x256 tiles %d..%d as %d tiles of 64x128, K in 4 quarters per "
+                     "workgroup", BITS, MPC, BF ? "bf16" : "f16", rg.tile0, rg.tile0 + rg.count - 1, blocks);
+        else
+            log_plan("gemm_ks_kernel<%d,%d,%s> M=%lld K=%lld N=%lld G=%d: %dx%d tiles of 64x128, K in 4 quarters "
+                     "per workgroup", BITS, MPC, BF ? "bf16" : "f16", (long long)M, (long long)L.K, (long long)L.N,
+                     L.group, tiles_m, tiles_n);
+    }
+    return launch(gemm_ks_kernel<BITS, MPC, BF>, dim3((unsigned)blocks), dim3(kKsThreads), 0, s, A, pk, C, (int)M,
+                  (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na, (int)L.ng, (int)L.np, tiles_m, tiles_n,
+                  rg);
 }
 
 template <int BITS, bool BF>
 int launch_ks_bits(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
-                   hipStream_t s) {
+                   const KsRange& rg, hipStream_t s) {
     const int chunk_rows = kKsBK * kKsCS;
     const int mpc = L.group >= chunk_rows ? 1 : chunk_rows / L.group;
-    if (mpc == 1) return launch_ks<BITS, 1, BF>(L, A, pk, C, M, s);
-    if (mpc == 2) return launch_ks<BITS, 2, BF>(L, A, pk, C, M, s);
-    return launch_ks<BITS, 4, BF>(L, A, pk, C, M, s);
+    if (mpc == 1) return launch_ks<BITS, 1, BF>(L, A, pk, C, M, rg, s);
+    if (mpc == 2) return launch_ks<BITS, 2, BF>(L, A, pk, C, M, rg, s);
+    return launch_ks<BITS, 4, BF>(L, A, pk, C, M, rg, s);
+}
+
+int launch_any(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M, const KsRange& rg,
+               hipStream_t s, bool bf) {
+    const uint8_t* pk = static_cast<const uint8_t*>(packed);
+    if (bf)
+        return L.bits == 4 ? launch_ks_bits<4, true>(L, A, pk, C, M, rg, s)
+                           : launch_ks_bits<8, true>(L, A, pk, C, M, rg, s);
+    return L.bits == 4 ? launch_ks_bits<4, false>(L, A, pk, C, M, rg, s)
+                       : launch_ks_bits<8, false>(L, A, pk, C, M, rg, s);
 }
 
 }  // namespace
@@ -492,10 +522,13 @@ bool gemm_ks_supported(const Layout& L) {
 
 int launch_gemm_ks(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                    hipStream_t s, bool bf) {
-    const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    if (bf)
-        return L.bits == 4 ? launch_ks_bits<4, true>(L, A, pk, C, M, s) : launch_ks_bits<8, true>(L, A, pk, C, M, s);
-    return L.bits == 4 ? launch_ks_bits<4, false>(L, A, pk, C, M, s) : launch_ks_bits<8, false>(L, A, pk, C, M, s);
+    return launch_any(L, A, packed, C, M, KsRange{0, 0, 0, 0, 0}, s, bf);
+}
+
+int launch_gemm_ks_range(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
+                         const KsRange& rg, hipStream_t s, bool bf) {
+    if (rg.count <= 0) return TF_OK;
+    return launch_any(L, A, packed, C, M, rg, s, bf);
 }
 
 }  // namespace tf

@@ -557,6 +557,14 @@ int launch_gemm256(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16
 bool gemm_ks_supported(const Layout& L);
 int launch_gemm_ks(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                    hipStream_t s, bool bf);
+// The same kernel over a range of the 256-row GEMM's 256 x 256 tiles: count
+// tiles from tile0 in that GEMM's order (row-major or column-major over
+// tiles_m x tiles_n), each as 8 tiles of 64 x 128.
+struct KsRange {
+    int tile0, count, tiles_m, tiles_n, col_major;
+};
+int launch_gemm_ks_range(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
+                         const KsRange& rg, hipStream_t s, bool bf);
 int launch_gemm(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                 void* ws, size_t ws_bytes, hipStream_t s, bool bf);
 int launch_silu_mul(const uint16_t* gu, int64_t M, int64_t N, uint16_t* h, hipStream_t s, bool bf);

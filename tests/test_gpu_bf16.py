@@ -188,6 +188,7 @@ GEMM_CASES = [
     (8, 512, 4096, 4096, 128), (8, 129, 1024, 264, 32), (8, 1024, 1024, 4096, 128),
     (8, 2048, 2048, 2048, 64),
     (8, 384, 1152, 4088, 64), (8, 420, 640, 3968, 32),                 # 64 x 128 GEMM, 8-bit, ragged N / M
+    (4, 1100, 512, 13304, 64),                                         # 256-row whole tiles + 64 x 128 rest
 ]
 
 

@@ -192,7 +192,10 @@ GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 2
                (8, 384, 1152, 4088, 64), (8, 420, 640, 3968, 32), (4, 65, 4096, 776, 128),
                # the 128-row GEMM: 4-bit beyond the 64 x 128 kernel's 1200 tiles, and
                # long K on few tiles (split-K)
-               (4, 1000, 1024, 10000, 128), (4, 200, 12288, 520, 128), (8, 100, 16384, 264, 64)]
+               (4, 1000, 1024, 10000, 128), (4, 200, 12288, 520, 128), (8, 100, 16384, 264, 64),
+               # 260 tiles of 256 x 256: one whole-tile round, the last 4 tiles (a partial
+               # row tile, ragged N) by the 64 x 128 kernel, some of its parts wholly past C
+               (4, 1100, 512, 13304, 64), (8, 1100, 1024, 13304, 128)]
 
 
 @pytest.mark.parametrize("bits,M,K,N,G", GEMM_SHAPES)
@@ -207,7 +210,8 @@ def test_gemm_parity_small(tf, bits, M, K, N, G):
                                              ("gemm", 8, 1024, 4096, 768), ("gemm", 4, 16, 4096, 1024),
                                              ("gemm", 8, 5, 8192, 512), ("gemm", 4, 64, 4096, 1024),
                                              ("gemm", 8, 33, 4096, 520), ("gemm", 4, 300, 8192, 520),
-                                             ("gemm", 8, 384, 512, 4096), ("gemm", 4, 200, 1024, 520)])
+                                             ("gemm", 8, 384, 512, 4096), ("gemm", 4, 200, 1024, 520),
+                                             ("gemm", 4, 1100, 512, 13304)])
 def test_integer_invariant_bitexact(tf, kind, bits, M, K, N):
     """s = 1, z = 0, integer x in [-3, 3]: every partial sum is an integer below
     2^24, so the fp16 output must be RNE of the exact integer matmul."""
