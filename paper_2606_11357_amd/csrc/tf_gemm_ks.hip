@@ -287,8 +287,9 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
             }
         }
     };
-    // Loads issued for step t (its metadata when it opens a group, its atoms,
-    // its A fragments): what a counted wait leaves in flight per step.
+    // Loads issued in the step that requests step t's operands: t's metadata
+    // when t opens a group, its atoms, and that step's four direct loads of A
+    // (half a pair): what a counted wait leaves in flight per step.
     auto loads_for = [&](int t) { return kKsRB + PANELS + (t % SPG == 0 ? 2 * PANELS : 0); };
     auto tie_meta = [&](Meta& mt) {
 #pragma unroll
