@@ -20,7 +20,7 @@ from paper_2606_11357_amd import tilefuse as tf
 from paper_2606_11357_amd.synth import make_inputs
 up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
 for bits, M, K, N in ((4, 2048, 4096, 14336), (4, 2048, 14336, 4096), (8, 512, 4096, 4096),
-                      (4, 1, 4096, 14336), (4, 16, 2048, 2048)):
+                      (4, 1, 4096, 14336), (4, 16, 2048, 2048), (4, 1280, 4096, 14336)):
     d = make_inputs(bits, 1, K, N, seed=0)
     if bits == 4:
         p = tf.pack_w4(up(d["qweight"]), up(d["qzeros"]), up(d["s"]), K, N)
@@ -47,14 +47,20 @@ def test_tf_log_names_each_plan():
         pytest.skip("no GPU")
     r = _run("1")
     assert r.returncode == 0 and "done" in r.stdout, r.stderr[-3000:]
-    lines = [ln for ln in r.stderr.splitlines() if ln.startswith("[tilefuse] ") and not ln.startswith("[tilefuse]   ")]
-    assert len(lines) == 5, r.stderr
+    all_lines = [ln for ln in r.stderr.splitlines() if ln.startswith("[tilefuse] ")]
+    lines = [ln for ln in all_lines if not ln.startswith("[tilefuse]   ")]
+    assert len(lines) == 6, r.stderr
     assert "gemm256_kernel<4,1,f16> M=2048 K=4096 N=14336" in lines[0]
     assert "gemm256_kernel<4,1,f16> M=2048 K=14336 N=4096" in lines[1]
     assert "stream-K" in lines[1]
     assert "gemm_ks_kernel<8," in lines[2] and "M=512" in lines[2]
     assert "gemv_kernel<4,1," in lines[3] and "vector form" in lines[3]
     assert "gemv_kernel<4,16," in lines[4] and "matrix-core form" in lines[4]
+    # 280 tiles of 256 x 256: one whole-tile round, the 24 after it on the K-split GEMM
+    assert "gemm256_kernel<4,1,f16> M=1280 K=4096 N=14336" in lines[5]
+    assert "K-split GEMM over the rest" in lines[5]
+    rest = all_lines[all_lines.index(lines[5]) + 1]
+    assert "gemm_ks_kernel<4,1,f16>" in rest and "tiles 256..279" in rest and "192 tiles of 64x128" in rest
 
 
 def test_silent_without_tf_log():
