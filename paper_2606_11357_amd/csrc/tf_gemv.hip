@@ -86,8 +86,12 @@ struct WaveStage {
 // atoms, fixed at compile time (one group of 32 SEG rows); SEG = 0: group
 // size known at run time.  D: weight atoms a wave keeps in flight; D = U is
 // the one-round form (the vector forms with at most U atoms per wave): every
-// atom of the run is requested at the start and nothing is refilled.
-template <int BITS, int M, int WAVES, int SEG, int D, bool BF>
+// atom of the run is requested at the start and nothing is refilled.  CH: the
+// workgroups that share one panel (vector forms, all of K each): workgroup
+// part h computes the columns c + 16 t with t in [h T / CH, (h + 1) T / CH),
+// reading only those columns' 16 / CH bytes of each lane's 16, so that few
+// panels still give every compute unit its own share of the weight stream.
+template <int BITS, int M, int WAVES, int SEG, int D, bool BF, int CH>
 __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
     int K, int N, int group, int64_t s_off, int64_t z_off, int na, int ng, int S, int AS, int RW,
@@ -103,6 +107,8 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     static_assert(SEG == 0 || U % SEG == 0, "segments tile a round");
     static_assert(U % D == 0, "the load ring tiles a round");
     constexpr bool ONE = D == U && !MF;
+    static_assert(CH == 1 || (!MF && T % CH == 0), "column parts split a lane's columns");
+    constexpr int TE = T / CH;                          // columns a lane computes
     // metadata of the groups one round touches: U / SEG groups, or up to U
     constexpr int NGR = SEG > 0 ? U / SEG : U;
     constexpr int SLANES = NGR * PW * 2 / 16, ZLANES = NGR * PW / 8;
@@ -123,7 +129,15 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     using Smem = std::conditional_t<MF, SmemShared, SmemApart>;
     __shared__ __align__(16) Smem sm;
 
-    const int p = blockIdx.x;
+    // With CH parts per panel, the parts of a panel are workgroups b, b + 8,
+    // ..., b + 8 (CH - 1): one XCD (workgroups are dealt to the eight XCDs in
+    // turn), so every part after the first finds the panel's lines in that
+    // XCD's L2.  Workgroups past the last panel (the grid is whole groups of
+    // 8 CH) end at once.
+    const int p = CH == 1 ? blockIdx.x : blockIdx.x / (8 * CH) * 8 + blockIdx.x % 8;
+    const int part_h = CH == 1 ? 0 : blockIdx.x / 8 % CH;
+    const int tp0 = part_h * TE;                        // first of this part's columns t of a lane
+    if (CH > 1 && p >= (N + PW - 1) / PW) return;
     const int split = blockIdx.y;                       // K-slice of this workgroup
     const int a_end = min(na, split * AS + AS);
     const int tid = threadIdx.x, lane = tid & 63;
@@ -138,7 +152,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     const int aw_end = min(a_end, aw0 + RW);
     const int nw = aw_end - aw0;                        // may be <= 0: an idle wave
     const int nrounds = nw > 0 ? (nw + U - 1) / U : 0;
-    const u32x4* wrun = reinterpret_cast<const u32x4*>(packed) + (int64_t)p * na * 64 + lane;
+    // a lane's share of an atom: 16 bytes, or the 16 / CH bytes of its part's columns
+    using WT = std::conditional_t<CH == 1, u32x4, std::conditional_t<CH == 2, u32x2, uint32_t>>;
+    const WT* wrun = reinterpret_cast<const WT*>(packed + ((int64_t)p * na * 64 + lane) * 16 + 16 / CH * part_h);
     const uint8_t* spanel = packed + s_off + (int64_t)p * ng * PW * 2;
     const uint8_t* zpanel = packed + z_off + (int64_t)p * ng * PW;
     const int64_t s_last = ((int64_t)ng * PW * 2 - 16);     // last 16-byte slot of the panel's scales
@@ -147,11 +163,11 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     const uint8_t* sbytes = reinterpret_cast<const uint8_t*>(st.s);
     const uint8_t* zbytes = reinterpret_cast<const uint8_t*>(st.z);
 
-    float y[M][T];
+    float y[M][TE];
 #pragma unroll
     for (int m = 0; m < M; ++m)
 #pragma unroll
-        for (int t = 0; t < T; ++t) y[m][t] = 0.f;
+        for (int t = 0; t < TE; ++t) y[m][t] = 0.f;
 
     // Loads.  A round is U atoms of the run; its small loads (the wave's
     // slice of x, its groups' metadata) are issued one round ahead.  Weight
@@ -187,9 +203,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
     // atom j of the run; requests past the run repeat its last atom (a cache
     // hit, issued without a branch for the same reason)
     auto load_atom = [&](int j) {
-        return __builtin_nontemporal_load(wrun + (int64_t)min(aw0 + min(j, nw - 1), na - 1) * 64);
+        return __builtin_nontemporal_load(wrun + (int64_t)min(aw0 + min(j, nw - 1), na - 1) * 64 * CH);
     };
-    u32x4 ring[D];
+    WT ring[D];
     // Matrix-core form: the A operand of v_mfma_f32_16x16x32_f16 for atom j
     // and row block b, row 16 b + c (row slots past mr repeat row mr - 1),
     // k = 32 a + 8 kg + 0..7, read straight from global memory (A is small
@@ -252,9 +268,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-        float acc[M][T];                 // factored form: sums of x * code of the open segment
+        float acc[M][TE];                // factored form: sums of x * code of the open segment
         float bo[M], sx[M];              // ... and the segment's sums of x * offset and of x
-        DqConst<BF> kq[T];               // dequant form: the open segment's scale and zero-point
+        DqConst<BF> kq[TE];              // dequant form: the open segment's scale and zero-point
         // matrix-core factored form: the open segment's sums of A x code and
         // of A (row sums, the same in every column of a block)
         float4_t accg[MFF ? MB : 1][MFF ? T : 1], rsum[MFF ? MB : 1];
@@ -272,13 +288,13 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                     bo[m] = 0.f;
                     sx[m] = 0.f;
 #pragma unroll
-                    for (int t = 0; t < T; ++t) acc[m][t] = 0.f;
+                    for (int t = 0; t < TE; ++t) acc[m][t] = 0.f;
                 }
             } else {
-                const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
-                const uint8_t* zp = zbytes + gl * PW + c * T;
+                const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T + tp0) * 2);
+                const uint8_t* zp = zbytes + gl * PW + c * T + tp0;
 #pragma unroll
-                for (int t = 0; t < T; ++t) kq[t] = make_dq_const<BF>(sp[t], zp[t]);
+                for (int t = 0; t < TE; ++t) kq[t] = make_dq_const<BF>(sp[t], zp[t]);
             }
         };
         // close the open segment: y += s * (acc - bo - z * sx); matrix-core
@@ -300,10 +316,10 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                             macc[b][t][q] = fmaf(sf, fmaf(-zo, rsum[b][q], accg[b][t][q]), macc[b][t][q]);
                 }
             } else if constexpr (FACT) {
-                const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T) * 2);
-                const uint8_t* zp = zbytes + gl * PW + c * T;
+                const uint16_t* sp = reinterpret_cast<const uint16_t*>(sbytes + (gl * PW + c * T + tp0) * 2);
+                const uint8_t* zp = zbytes + gl * PW + c * T + tp0;
 #pragma unroll
-                for (int t = 0; t < T; ++t) {
+                for (int t = 0; t < TE; ++t) {
                     const float zf = (float)zp[t];
                     const float sf = scale_f32<BF>(sp[t]);
 #pragma unroll
@@ -319,7 +335,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
             const int j = r * U + i;      // atom of the run
             if (i > 0 && j >= nw) break;
             // take atom j from the ring and request atom j + D in its place
-            const u32x4 wv = ring[i % D];
+            const WT wv = ring[i % D];
             if constexpr (!ONE) ring[i % D] = load_atom(j + D);
             u32x4 afrag[MF ? MB : 1];
             if constexpr (MF) {
@@ -352,9 +368,17 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
                     sx[m] += v[1];
                 }
             }
-            const uint32_t wd[4] = {wv[0], wv[1], wv[2], wv[3]};
+            // the dwords of this part's columns (dword t of a 4-bit lane is
+            // column t, dwords 2 t and 2 t + 1 of an 8-bit lane are column t)
+            uint32_t wd[4 / CH];
+            if constexpr (CH == 4) {
+                wd[0] = wv;
+            } else {
 #pragma unroll
-            for (int t = 0; t < T; ++t) {
+                for (int q = 0; q < 4 / CH; ++q) wd[q] = wv[q];
+            }
+#pragma unroll
+            for (int t = 0; t < TE; ++t) {
                 uint32_t P[4];
                 if constexpr (MFF) {
                     // the codes as exact 16-bit integers o + q: fp16 1024 + q,
@@ -484,7 +508,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 #pragma unroll
         for (int m = 0; m < M; ++m)
 #pragma unroll
-            for (int t = 0; t < T; ++t) {
+            for (int t = 0; t < TE; ++t) {
                 float v = y[m][t];
                 v += __shfl_xor(v, 16);
                 v += __shfl_xor(v, 32);
@@ -494,13 +518,14 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 #pragma unroll
             for (int m = 0; m < M; ++m)
 #pragma unroll
-                for (int t = 0; t < T; ++t) sm.red[wave][m][c + 16 * t] = y[m][t];
+                for (int t = 0; t < TE; ++t) sm.red[wave][m][c + 16 * (tp0 + t)] = y[m][t];
         }
     }
     __syncthreads();
-    if (S == 1) {
-        for (int i = tid; i < M * PW; i += NT) {
-            const int m = i / PW, col = i % PW;
+    if (CH > 1 || S == 1) {
+        // this part's columns: c + 16 t for t in [tp0, tp0 + TE), PW / CH in a row
+        for (int i = tid; i < M * PW / CH; i += NT) {
+            const int m = i / (PW / CH), col = i % (PW / CH) + 16 * tp0;
             const int n = p * PW + col;
             if (n < N && m < mr) {
                 float v = 0.f;
@@ -555,7 +580,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(
 // timings of both forms on MI355X (e.g. K=4096 with 64 or 128 panels at M=1:
 // one pass is faster; K=14336 with 64 panels: the split is).
 struct GemvPlan {
-    int waves, S, AS;
+    int waves, S, AS, CH;
 };
 constexpr int kMaxSplit = 32;
 constexpr int64_t kSplitBelowPanels = 192;      // split K only below this many panels ...
@@ -575,8 +600,35 @@ constexpr int gemv_waves_for(int M) { return M <= 3 ? 16 : 8; }
 // W4 10%, N=4096 W8 11% faster).
 constexpr int gemv_ring_for(int) { return 2; }
 
+// Column parts per panel (vector forms): 2 or 4 workgroups share a panel,
+// each reading only its own columns' bytes of every atom over all of K, so
+// that few panels still give every compute unit a share of the stream and of
+// the dot products, with no partial sums.  Taken while panels x parts fit one
+// workgroup per compute unit, for runs of up to kPartsMaxAtoms atoms carrying
+// at least kPartsFromWork work (the K split's measure): every part requests
+// all of the panel's cache lines, so over long runs a compute unit's line
+// rate, not the bytes it uses, sets the time and the K split is faster, and
+// on short light runs the extra workgroups only add start-up time.  Measured
+// on MI355X (graph replay, against the plan without parts): K = N = 4096,
+// W4 M = 1, 4, 8 5.84, 8.66, 12.8 -> 5.66, 7.64, 8.4 us, W8 M = 8 10.5 ->
+// 8.6 us; K = 14336, N = 4096 W4 M = 1 13.2 us with 4 parts against 10.0 us
+// split; two workgroups per compute unit (K = 4096, N = 14336, M = 1 to 8)
+// 1-21% slower.
+constexpr int64_t kPartsMaxAtoms = 128;
+constexpr int64_t kPartsFromWork = 128;
+inline int gemv_parts(const Layout& L, int64_t M) {
+    if (M > TF_GEMV_MAX_M || L.na > kPartsMaxAtoms || L.na * std::max<int64_t>(1, M / 2) < kPartsFromWork)
+        return 1;
+    const int64_t T = L.pw / 16;
+    int ch = 1;
+    while (2 * ch <= T && L.np * 2 * ch <= kTargetWorkgroups) ch *= 2;
+    return ch;
+}
+
 inline GemvPlan plan_gemv(const Layout& L, int64_t M) {
     const int waves = gemv_waves_for((int)M);
+    const int CH = gemv_parts(L, M);
+    if (CH > 1) return {waves, 1, (int)L.na, CH};
     // slices keep at least this many atoms: a round of 16 waves at M = 1, of
     // 8 up to 8 rows; the matrix-core form (little vector work per atom)
     // splits down to kMfSliceAtoms
@@ -592,7 +644,7 @@ inline GemvPlan plan_gemv(const Layout& L, int64_t M) {
     int64_t AS = (L.na + S - 1) / S;
     AS = (AS + apg - 1) / apg * apg;     // slices start on group boundaries
     S = (L.na + AS - 1) / AS;            // no empty slice
-    return {waves, (int)S, (int)AS};
+    return {waves, (int)S, (int)AS, 1};
 }
 
 // Workspace layout: arrival counters first, at a fixed place and sized for
@@ -612,20 +664,30 @@ int launch_g(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C,
     const int AS = split ? sp.AS : (int)L.na;
     int RW = (AS + WAVES - 1) / WAVES;               // atoms per wave
     if (SEG > 0) RW = (RW + SEG - 1) / SEG * SEG;    // runs start on group boundaries
-    auto go = [&](auto kernel, int d) {
+    auto go = [&](auto kernel, int d, int ch) {
         if (log_enabled())
-            log_plan("gemv_kernel<%d,%d,%d,%d,%d,%s> rows=%d K=%lld N=%lld G=%d: %s form, %lld panels x %d K "
-                     "slices of %d atoms, %d atoms per wave%s", BITS, M, WAVES, SEG, d, BF ? "bf16" : "f16", mr,
-                     (long long)L.K, (long long)L.N, L.group,
+            log_plan("gemv_kernel<%d,%d,%d,%d,%d,%s,%d> rows=%d K=%lld N=%lld G=%d: %s form, %lld panels x %d "
+                     "column parts x %d K slices of %d atoms, %d atoms per wave%s", BITS, M, WAVES, SEG, d,
+                     BF ? "bf16" : "f16", ch, mr, (long long)L.K, (long long)L.N, L.group,
                      M > TF_GEMV_MAX_M ? "matrix-core" : (d == kGemvU ? "one-round vector" : "vector"),
-                     (long long)L.np, S, AS, RW, split ? ", partials summed by the last slice" : "");
-        return launch(kernel, dim3((unsigned)L.np, (unsigned)S), dim3(WAVES * 64), 0, s, A, pk, C,
+                     (long long)L.np, ch, S, AS, RW, split ? ", partials summed by the last slice" : "");
+        // column parts: whole groups of 8 ch workgroups (those past the last panel end at once)
+        const int64_t gx = ch == 1 ? L.np : (L.np + 7) / 8 * 8 * ch;
+        return launch(kernel, dim3((unsigned)gx, (unsigned)S), dim3(WAVES * 64), 0, s, A, pk, C,
                       (int)L.K, (int)L.N, L.group, L.s_off, L.z_off, (int)L.na, (int)L.ng, S, AS, RW,
                       part, cnt, mr);
     };
-    if constexpr (M <= TF_GEMV_MAX_M)
-        if (RW <= kGemvU) return go(gemv_kernel<BITS, M, WAVES, SEG, kGemvU, BF>, kGemvU);
-    return go(gemv_kernel<BITS, M, WAVES, SEG, gemv_ring_for(M), BF>, gemv_ring_for(M));
+    auto with_parts = [&](auto ch_tag) {
+        constexpr int CH = decltype(ch_tag)::value;
+        if (RW <= kGemvU) return go(gemv_kernel<BITS, M, WAVES, SEG, kGemvU, BF, CH>, kGemvU, CH);
+        return go(gemv_kernel<BITS, M, WAVES, SEG, gemv_ring_for(M), BF, CH>, gemv_ring_for(M), CH);
+    };
+    if constexpr (M <= TF_GEMV_MAX_M) {
+        if (BITS == 4 && sp.CH == 4) return with_parts(std::integral_constant<int, BITS == 4 ? 4 : 1>{});
+        if (sp.CH == 2) return with_parts(std::integral_constant<int, 2>{});
+        return with_parts(std::integral_constant<int, 1>{});
+    }
+    return go(gemv_kernel<BITS, M, WAVES, SEG, gemv_ring_for(M), BF, 1>, gemv_ring_for(M), 1);
 }
 
 template <int BITS, int M, bool BF>
