@@ -3,7 +3,8 @@
 // microkernel"; Section 4.4):
 //   C[M, N] = A[M, K] x dequant(packed)[K, N], fp16 or bf16 MFMA, fp32 sums.
 //
-// Workgroup tile 64 x 128, four waves, one per SIMD.  Each wave computes the
+// Workgroup tile 64 x BN (BN = 128, or 256 for 4-bit weights where the
+// wider tiles still fill the chip), four waves, one per SIMD.  Each wave computes the
 // whole tile over its own quarter of K (a contiguous run of 128-row chunks),
 // and no partial sum leaves the compute unit; inside the loop the waves share
 // nothing and never wait for each other.
@@ -18,7 +19,7 @@
 //    of a group travels with the atoms of the step that opens it.  All loads
 //    are asm statements with counted waits, issued metadata, atoms, A in the
 //    order their waits need them (vector-memory loads complete in order).
-//  - A step's 32 MFMAs run column block by column block (8 blocks of 16
+//  - A step's MFMAs run column block by column block (BN / 16 blocks of 16
 //    columns, each against the 4 row blocks); while the four MFMAs of block u
 //    run, the wave dequantizes (Eq. 2, rounded once, the same arithmetic as
 //    the other GEMMs) the B operand of block u + 1, so the dequantization's
@@ -37,12 +38,12 @@
 namespace tf {
 namespace {
 
-constexpr int kKsBM = 64, kKsBN = 128, kKsBK = 32;
+constexpr int kKsBM = 64, kKsBK = 32;
 constexpr int kKsWaves = 4, kKsThreads = 64 * kKsWaves;
 constexpr int kKsCS = 4;                // steps per chunk (128 rows of K) and ring slots
 constexpr int kKsLead = 3;              // steps between a request and its step
 constexpr int kKsRB = kKsBM / 16;       // row blocks
-constexpr int kKsNB = kKsBN / 16;       // column blocks: B operands per step
+constexpr int kKsSumNB = 8;             // column blocks per pass of the quarters' sum
 constexpr int kKsXcds = 8;
 constexpr int kKsRing = 4;              // A buffers per wave, one pair of steps each
 constexpr int kKsPairBytes = kKsBM * 2 * kKsBK * 2;   // 64 rows x 128 bytes
@@ -61,19 +62,20 @@ constexpr int kKsMetaSlot = 0, kKsAtomSlot = 4, kKsASlot = 8, kKsASlotStride = 3
 // old constants were last used under block v - 1).
 constexpr int kKsMetaWaitBlock = 5;
 constexpr int kKsReadSlot = 24;         // the next step's fragments, after that wait
-constexpr int kKsConstSlot[8] = {20, 21, 22, 23, 24, 25, 26, 28};
+constexpr int kKsConstSlot[16] = {20, 21, 22, 23, 24, 25, 26, 28, 32, 36, 40, 44, 48, 52, 56, 60};
 static_assert(kKsMetaSlot < kKsAtomSlot && kKsAtomSlot < kKsASlot, "requests go out metadata, atoms, A");
 static_assert(kKsASlot + kKsASlotStride * (kKsRB - 1) < kKsMetaWaitBlock * kKsRB,
               "a step's requests are all issued before its second wait counts them");
-constexpr bool ks_const_slots_ok() {
-    for (int v = 0; v < kKsNB; ++v) {
+constexpr bool ks_const_slots_ok(int nb) {
+    for (int v = 0; v < nb; ++v) {
         const int blk = kKsConstSlot[v] / kKsRB;
-        if (blk < kKsMetaWaitBlock || blk < v || blk >= kKsNB) return false;
+        if (blk < kKsMetaWaitBlock || blk < v || blk >= nb) return false;
     }
     return true;
 }
-static_assert(ks_const_slots_ok(), "constants formed after the wait and after their old value's last use");
-static_assert(kKsReadSlot >= kKsMetaWaitBlock * kKsRB && kKsReadSlot < kKsNB * kKsRB,
+static_assert(ks_const_slots_ok(8) && ks_const_slots_ok(16),
+              "constants formed after the wait and after their old value's last use");
+static_assert(kKsReadSlot >= kKsMetaWaitBlock * kKsRB && kKsReadSlot < 8 * kKsRB,
               "the next step's fragments are read after the wait that completes their pair");
 // The pair holding step s + 1 was requested during steps up to
 // 2 (kKsALead - 1) before it, which the wait at step s completes when that is
@@ -147,21 +149,24 @@ __device__ __forceinline__ u32x4 ds_read16(uint32_t addr) {
 __device__ __forceinline__ void lgkm_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 // MPC: metadata groups per chunk (1 when a group spans the chunk, else chunk
-// rows / group).
-template <int BITS, int MPC, bool BF>
+// rows / group).  BN: tile columns.
+template <int BITS, int MPC, bool BF, int BN>
 __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     const uint16_t* __restrict__ A, const uint8_t* __restrict__ packed, uint16_t* __restrict__ C,
     int M, int K, int N, int gshift, int64_t s_off, int64_t z_off, int na, int ng, int np,
     int tiles_m, int tiles_n, KsRange rg) {
     constexpr int PW = BITS == 4 ? 64 : 32;   // columns per panel (one atom per step)
     constexpr int T = PW / 16;                // column blocks per panel
-    constexpr int PANELS = kKsBN / PW;
+    constexpr int PANELS = BN / PW;
+    constexpr int NB = BN / 16;               // column blocks: B operands per step
+    static_assert(BN == 128 || (BN == 256 && BITS == 4), "tiles of 64 x 128, or 64 x 256 for 4-bit weights");
     constexpr int SPG = kKsCS / MPC;          // steps per metadata group
     constexpr int S = dq_steps<BF, BITS>();   // dequantization micro-steps per operand
     static_assert(kKsRB + 2 * (kKsRB + 3 * PANELS) <= 40, "counted waits stay within vm_wait's range");
-    // A's per-wave rings during the loop; the K quarters' sums after it
-    // (wave w's quarter of the sum buffer is exactly its own ring)
-    __shared__ __align__(16) float4_t lds[kKsWaves][kKsRB * kKsNB][64];
+    // A's per-wave rings during the loop; the K quarters' sums after it, in
+    // passes of 8 column blocks (wave w's quarter of the sum buffer is exactly
+    // its own ring)
+    __shared__ __align__(16) float4_t lds[kKsWaves][kKsRB * kKsSumNB][64];
     static_assert(sizeof(lds) == kKsWaves * kKsRing * kKsPairBytes, "ring and sum buffer coincide");
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -171,10 +176,11 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
 
     // Block b runs on XCD b % 8, which takes the (b % 8)-th contiguous band
     // of the tile list: all tiles with row tiles varying fastest, or, over a
-    // range of 256 x 256 tiles, the 8 tiles of 64 x 128 of each in turn.
+    // range of 256 x 256 tiles, the UPT tiles of 64 x BN of each in turn.
+    constexpr int CPT = 256 / BN, UPT = 4 * CPT;
     int unit;
     {
-        const int total = rg.count ? rg.count * 8 : tiles_m * tiles_n;
+        const int total = rg.count ? rg.count * UPT : tiles_m * tiles_n;
         const int b = blockIdx.x;
         const int per = total / kKsXcds, rem = total % kKsXcds;
         const int x = b % kKsXcds, i = b / kKsXcds;
@@ -185,17 +191,17 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     // uniform would be loaded lane by lane)
     int tm, tn;
     if (rg.count) {
-        const int t = rg.tile0 + unit / 8, sub = unit % 8;
+        const int t = rg.tile0 + unit / UPT, sub = unit % UPT;
         const int tm2 = rg.col_major ? t % rg.tiles_m : t / rg.tiles_n;
         const int tn2 = rg.col_major ? t / rg.tiles_m : t % rg.tiles_n;
-        tm = __builtin_amdgcn_readfirstlane(4 * tm2 + sub / 2);
-        tn = __builtin_amdgcn_readfirstlane(2 * tn2 + sub % 2);
+        tm = __builtin_amdgcn_readfirstlane(4 * tm2 + sub / CPT);
+        tn = __builtin_amdgcn_readfirstlane(CPT * tn2 + sub % CPT);
     } else {
         tm = __builtin_amdgcn_readfirstlane(unit % tiles_m);
         tn = __builtin_amdgcn_readfirstlane(unit / tiles_m);
     }
-    const int64_t row0 = (int64_t)tm * kKsBM, col0 = (int64_t)tn * kKsBN;
-    // a 64 x 128 part of a 256 x 256 tile can lie wholly past C (the whole
+    const int64_t row0 = (int64_t)tm * kKsBM, col0 = (int64_t)tn * BN;
+    // a 64 x BN part of a 256 x 256 tile can lie wholly past C (the whole
     // workgroup leaves before any load or barrier)
     if (row0 >= M || col0 >= N) return;
 
@@ -326,11 +332,11 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
         dq_step<BF, BITS>(k, sl.w[pp][BITS == 4 ? t : 2 * t], sl.w[pp][BITS == 4 ? t : 2 * t + 1], magic, kq, st);
     };
 
-    float4_t acc[kKsRB][kKsNB];
+    float4_t acc[kKsRB][NB];
 #pragma unroll
     for (int i = 0; i < kKsRB; ++i)
 #pragma unroll
-        for (int u = 0; u < kKsNB; ++u) acc[i][u] = float4_t{0.f, 0.f, 0.f, 0.f};
+        for (int u = 0; u < NB; ++u) acc[i][u] = float4_t{0.f, 0.f, 0.f, 0.f};
 
     // Prologue: the requests of steps -6 .. -1 in the loop's order (the
     // direct loads of pairs 0 and 1 and half of 2... as steps -6 .. -4 issue
@@ -356,9 +362,9 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     tie_slot(ring[0]);
     u32x4 af[2][kKsRB];
     read_af(0, af[0]);
-    DqConst<BF> kc[kKsNB];
+    DqConst<BF> kc[NB];
 #pragma unroll
-    for (int u = 0; u < kKsNB; ++u) kc[u] = make_const(meta[0], u);
+    for (int u = 0; u < NB; ++u) kc[u] = make_const(meta[0], u);
     u32x4 bop[2];
     {
         DqSt<BF> st;
@@ -370,7 +376,7 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
 #pragma unroll
     for (int i = 0; i < kKsRB; ++i)
 #pragma unroll
-        for (int u = 0; u < kKsNB; ++u) asm volatile("" : "+a"(acc[i][u]));
+        for (int u = 0; u < NB; ++u) asm volatile("" : "+a"(acc[i][u]));
     mfma_hazard_gap();
 
     for (int ch = 0; ch < chunks; ++ch) {
@@ -382,11 +388,11 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
             const bool new_group = (j + 1) % SPG == 0;     // step + 1 opens a group
             const int jn = (j + 1) % kKsCS;                // ring slot of step + 1
 #pragma unroll
-            for (int u = 0; u < kKsNB; ++u) {
+            for (int u = 0; u < NB; ++u) {
                 // operand dequantized under block u: block u + 1 of this step,
                 // or block 0 of the next step under the last block
-                const int du = (u + 1) % kKsNB;
-                const Slot& src = ring[u + 1 < kKsNB ? j : jn];
+                const int du = (u + 1) % NB;
+                const Slot& src = ring[u + 1 < NB ? j : jn];
                 DqSt<BF> st;
 #pragma unroll
                 for (int i = 0; i < kKsRB; ++i) {
@@ -423,7 +429,7 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
                     // constants of the group step + 1 opens; block v's old
                     // ones were last used under block v - 1
 #pragma unroll
-                    for (int v = 0; v < kKsNB; ++v)
+                    for (int v = 0; v < NB; ++v)
                         if (new_group && q == kKsConstSlot[v]) kc[v] = make_const(meta[jn / SPG], v);
 #pragma unroll
                     for (int k = i * S / kKsRB; k < (i + 1) * S / kKsRB; ++k) dq_micro(k, src, du, kc[du], st);
@@ -448,70 +454,100 @@ __global__ __launch_bounds__(kKsThreads, 1) void gemm_ks_kernel(
     for (int m = 0; m < MPC; ++m) tie_meta(meta[m]);
     mfma_hazard_gap();
 
-    // Sum the four K quarters in quarter order: every wave parks its sums,
-    // then wave w adds row block w of all four and stores it.
-#pragma unroll
-    for (int i = 0; i < kKsRB; ++i)
-#pragma unroll
-        for (int u = 0; u < kKsNB; ++u) lds[wave][i * kKsNB + u][lane] = acc[i][u];
-    __syncthreads();
+    // Sum the four K quarters in quarter order, 8 column blocks per pass:
+    // every wave parks its sums, then wave w adds row block w of all four and
+    // stores it.
     const int i = wave;
     const int64_t row = row0 + 16 * i + c;
 #pragma unroll
-    for (int u = 0; u < kKsNB; ++u) {
-        const int b = i * kKsNB + u;
-        float4_t v = lds[0][b][lane];
+    for (int h = 0; h < NB / kKsSumNB; ++h) {
+        if (h > 0) __syncthreads();     // the previous pass's sums have been read
 #pragma unroll
-        for (int w = 1; w < kKsWaves; ++w) v += lds[w][b][lane];
-        // weights were the first MFMA operand: lane holds row c of the block
-        // and columns 4 kg .. 4 kg + 3 (N % 8 == 0, so all four or none fit)
-        const int64_t col = col0 + 16 * u + 4 * kg;
-        if (row < M && col < N) {
-            const uint2 o{round_out2<BF>(v[0], v[1]), round_out2<BF>(v[2], v[3])};
-            *reinterpret_cast<uint2*>(C + row * N + col) = o;
+        for (int r = 0; r < kKsRB; ++r)
+#pragma unroll
+            for (int u = 0; u < kKsSumNB; ++u) lds[wave][r * kKsSumNB + u][lane] = acc[r][h * kKsSumNB + u];
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < kKsSumNB; ++u) {
+            const int b = i * kKsSumNB + u;
+            float4_t v = lds[0][b][lane];
+#pragma unroll
+            for (int w = 1; w < kKsWaves; ++w) v += lds[w][b][lane];
+            // weights were the first MFMA operand: lane holds row c of the
+            // block and columns 4 kg .. 4 kg + 3 (N % 8 == 0, so all four or
+            // none fit)
+            const int64_t col = col0 + 16 * (h * kKsSumNB + u) + 4 * kg;
+            if (row < M && col < N) {
+                const uint2 o{round_out2<BF>(v[0], v[1]), round_out2<BF>(v[2], v[3])};
+                *reinterpret_cast<uint2*>(C + row * N + col) = o;
+            }
         }
     }
 }
 
-template <int BITS, int MPC, bool BF>
+template <int BITS, int MPC, bool BF, int BN>
 int launch_ks(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M, const KsRange& rg,
               hipStream_t s) {
     const int tiles_m = (int)((M + kKsBM - 1) / kKsBM);
-    const int tiles_n = (int)((L.N + kKsBN - 1) / kKsBN);
+    const int tiles_n = (int)((L.N + BN - 1) / BN);
     const int gshift = __builtin_ctz((unsigned)L.group);
-    const int blocks = rg.count ? rg.count * 8 : tiles_m * tiles_n;
+    const int blocks = rg.count ? rg.count * 4 * (256 / BN) : tiles_m * tiles_n;
     if (log_enabled()) {
         if (rg.count)
-            log_plan("  gemm_ks_kernel<%d,%d,%s>: 256x256 tiles %d..%d as %d tiles of 64x128, K in 4 quarters per "
-                     "workgroup", BITS, MPC, BF ? "bf16" : "f16", rg.tile0, rg.tile0 + rg.count - 1, blocks);
+            log_plan("  gemm_ks_kernel<%d,%d,%s,%d>: 256x256 tiles %d..%d as %d tiles of 64x%d, K in 4 quarters "
+                     "per workgroup", BITS, MPC, BF ? "bf16" : "f16", BN, rg.tile0, rg.tile0 + rg.count - 1, blocks,
+                     BN);
         else
-            log_plan("gemm_ks_kernel<%d,%d,%s> M=%lld K=%lld N=%lld G=%d: %dx%d tiles of 64x128, K in 4 quarters "
-                     "per workgroup", BITS, MPC, BF ? "bf16" : "f16", (long long)M, (long long)L.K, (long long)L.N,
-                     L.group, tiles_m, tiles_n);
+            log_plan("gemm_ks_kernel<%d,%d,%s,%d> M=%lld K=%lld N=%lld G=%d: %dx%d tiles of 64x%d, K in 4 quarters "
+                     "per workgroup", BITS, MPC, BF ? "bf16" : "f16", BN, (long long)M, (long long)L.K,
+                     (long long)L.N, L.group, tiles_m, tiles_n, BN);
     }
-    return launch(gemm_ks_kernel<BITS, MPC, BF>, dim3((unsigned)blocks), dim3(kKsThreads), 0, s, A, pk, C, (int)M,
-                  (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na, (int)L.ng, (int)L.np, tiles_m, tiles_n,
-                  rg);
+    return launch(gemm_ks_kernel<BITS, MPC, BF, BN>, dim3((unsigned)blocks), dim3(kKsThreads), 0, s, A, pk, C,
+                  (int)M, (int)L.K, (int)L.N, gshift, L.s_off, L.z_off, (int)L.na, (int)L.ng, (int)L.np, tiles_m,
+                  tiles_n, rg);
 }
 
-template <int BITS, bool BF>
+template <int BITS, bool BF, int BN>
 int launch_ks_bits(const Layout& L, const uint16_t* A, const uint8_t* pk, uint16_t* C, int64_t M,
                    const KsRange& rg, hipStream_t s) {
     const int chunk_rows = kKsBK * kKsCS;
     const int mpc = L.group >= chunk_rows ? 1 : chunk_rows / L.group;
-    if (mpc == 1) return launch_ks<BITS, 1, BF>(L, A, pk, C, M, rg, s);
-    if (mpc == 2) return launch_ks<BITS, 2, BF>(L, A, pk, C, M, rg, s);
-    return launch_ks<BITS, 4, BF>(L, A, pk, C, M, rg, s);
+    if (mpc == 1) return launch_ks<BITS, 1, BF, BN>(L, A, pk, C, M, rg, s);
+    if (mpc == 2) return launch_ks<BITS, 2, BF, BN>(L, A, pk, C, M, rg, s);
+    return launch_ks<BITS, 4, BF, BN>(L, A, pk, C, M, rg, s);
+}
+
+// 64 x 256 tiles (4-bit weights only): twice the MFMA work per byte a
+// compute unit loads, at about 1.5 times a 64 x 128 tile's time (one round of
+// either at K = 4096, N = 14336: 32.4 against 21.4 us).  Taken when whole
+// rounds of them at that cost beat the 64 x 128 tiles' rounds counted
+// fractionally (a short last round of small tiles runs faster than a full
+// one).  Measured on MI355X (graph replay, fp16; 64 x 128 -> 64 x 256):
+// K = 4096, N = 14336, M = 256 and 512 41.2 -> 37.0 and 80.5 -> 70.3 us;
+// K = 4096, N = 4096, M = 1000 43.3 -> 38.7 us; K = 4096, N = 11008, M = 300
+// 40.0 -> 35.2 us; left at 64 x 128: N = 14336, M = 128, 384, 640 (21.4, 61,
+// 100 against 32.4, 67, 103.5 us) and K = 8192, N = 8192, M = 200 (39.2
+// against 56 us).
+constexpr int64_t kKsWideCostHalves = 3;    // a 64 x 256 tile's time in halves of a 64 x 128 tile's
+bool gemm_ks_wide(const Layout& L, int64_t M, hipStream_t s) {
+    if (L.bits != 4) return false;
+    const int64_t cus = device_cus(s);
+    const int64_t tm = (M + 63) / 64;
+    const int64_t t128 = tm * ((L.N + 127) / 128), t256 = tm * ((L.N + 255) / 256);
+    return 2 * t128 > kKsWideCostHalves * ((t256 + cus - 1) / cus) * cus;
 }
 
 int launch_any(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M, const KsRange& rg,
-               hipStream_t s, bool bf) {
+               hipStream_t s, bool bf, bool wide) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    if (bf)
-        return L.bits == 4 ? launch_ks_bits<4, true>(L, A, pk, C, M, rg, s)
-                           : launch_ks_bits<8, true>(L, A, pk, C, M, rg, s);
-    return L.bits == 4 ? launch_ks_bits<4, false>(L, A, pk, C, M, rg, s)
-                       : launch_ks_bits<8, false>(L, A, pk, C, M, rg, s);
+    if (L.bits == 8)
+        return bf ? launch_ks_bits<8, true, 128>(L, A, pk, C, M, rg, s)
+                  : launch_ks_bits<8, false, 128>(L, A, pk, C, M, rg, s);
+    if (wide)
+        return bf ? launch_ks_bits<4, true, 256>(L, A, pk, C, M, rg, s)
+                  : launch_ks_bits<4, false, 256>(L, A, pk, C, M, rg, s);
+    return bf ? launch_ks_bits<4, true, 128>(L, A, pk, C, M, rg, s)
+              : launch_ks_bits<4, false, 128>(L, A, pk, C, M, rg, s);
 }
 
 }  // namespace
@@ -523,13 +559,13 @@ bool gemm_ks_supported(const Layout& L) {
 
 int launch_gemm_ks(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                    hipStream_t s, bool bf) {
-    return launch_any(L, A, packed, C, M, KsRange{0, 0, 0, 0, 0}, s, bf);
+    return launch_any(L, A, packed, C, M, KsRange{0, 0, 0, 0, 0}, s, bf, gemm_ks_wide(L, M, s));
 }
 
 int launch_gemm_ks_range(const Layout& L, const uint16_t* A, const void* packed, uint16_t* C, int64_t M,
                          const KsRange& rg, hipStream_t s, bool bf) {
     if (rg.count <= 0) return TF_OK;
-    return launch_any(L, A, packed, C, M, rg, s, bf);
+    return launch_any(L, A, packed, C, M, rg, s, bf, false);
 }
 
 }  // namespace tf

@@ -2,16 +2,16 @@
 
 Both MFMA GEMMs issue their matrix instructions as asm statements with
 AGPR-pinned accumulators, so the compiler inserts none of the wait states the
-ISA requires around them; the 64 x 128 GEMM also issues its buffer loads as
+ISA requires around them; the K-split GEMM also issues its buffer loads as
 asm statements and waits for them with its own counted s_waitcnt, so the
 compiler inserts none of those waits either.  These tests compile the two
 kernel files to gfx950 assembly with the library's own flags and check every
 instantiation:
 
-  * 64 x 128 GEMM: no VGPR that a buffer load targets is read or overwritten
-    before a wait that leaves that load complete (vector-memory loads complete
-    in issue order), over the prologue, three passes of the step loop and the
-    epilogue;
+  * K-split GEMM (64 x 128 and 64 x 256 tiles): no VGPR that a buffer load
+    targets is read or overwritten before a wait that leaves that load
+    complete (vector-memory loads complete in issue order), over the
+    prologue, three passes of the step loop and the epilogue;
   * both GEMMs: at least two wait states between a vector-ALU write of an MFMA's
     A or B operand and the MFMA, and between an accumulator write
     (v_accvgpr_write) and an MFMA reading it; at least 18 between an MFMA
@@ -200,7 +200,8 @@ def check_mfma_hazards(seq):
 
 def test_ks_counted_waits(asm):
     fns = functions(asm["tf_gemm_ks.hip"], KERNELS["tf_gemm_ks.hip"])
-    assert len(fns) == 12                       # 4/8-bit x 1/2/4 groups per chunk x fp16/bf16
+    # 1/2/4 groups per chunk x fp16/bf16 x (4-bit: 64 x 128 and 64 x 256 tiles, 8-bit: 64 x 128)
+    assert len(fns) == 18
     for name, ins in fns:
         lp = loops(ins)
         assert len(lp) == 1, name               # one step loop, no waterfall loops
@@ -210,10 +211,13 @@ def test_ks_counted_waits(asm):
         assert check_vm_waits(seq) == [], name
 
 
+INSTANTIATIONS = {"tf_gemm_ks.hip": 18, "tf_gemm256.hip": 12}
+
+
 @pytest.mark.parametrize("f", sorted(KERNELS))
 def test_mfma_wait_states(asm, f):
     fns = functions(asm[f], KERNELS[f])
-    assert len(fns) == 12
+    assert len(fns) == INSTANTIATIONS[f]
     for name, ins in fns:
         assert sum(op.startswith("v_mfma") for op, _, _ in ins) >= 64, name
         assert check_mfma_hazards(code(ins)) == [], name

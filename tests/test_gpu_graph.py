@@ -20,6 +20,7 @@ pytestmark = pytest.mark.gpu
 CASES = [("gemm", 4, 1100, 1024, 2320),   # 256-row tiles, stream-K
          ("gemm", 4, 200, 12288, 520),    # 128-row tiles, split-K
          ("gemm", 4, 200, 1024, 520),     # 64 x 128 tiles, K over the waves
+         ("gemm", 4, 512, 512, 14336),    # 64 x 256 tiles, K over the waves
          ("gemm", 4, 40, 4096, 1024),     # streaming matrix-core form, 64 row slots
          ("gemm", 4, 20, 14336, 4096),    # streaming matrix-core form, factored, K split
          ("gemv", 4, 1, 14336, 4096),     # decode GEMV, K split

@@ -32,6 +32,10 @@ for bits, M, K, N in ((4, 2048, 4096, 14336), (4, 2048, 14336, 4096), (8, 512, 4
 d = make_inputs(8, 1, 4096, 4096, seed=0)
 p = tf.pack_w8(up(d["qweight"]), up(d["zeros"]), up(d["s"]), 4096, 4096)
 tf.w8a16_gemv(torch.zeros((8, 4096), dtype=torch.float16, device="cuda"), p, 4096, 4096)
+# prefill below 1024 rows: 64 x 256 tiles of the K-split GEMM
+d = make_inputs(4, 1, 4096, 14336, seed=0)
+p = tf.pack_w4(up(d["qweight"]), up(d["qzeros"]), up(d["s"]), 4096, 14336)
+tf.w4a16_gemm(torch.zeros((512, 4096), dtype=torch.float16, device="cuda"), p, 4096, 14336)
 torch.cuda.synchronize()
 print("done")
 """
@@ -53,19 +57,20 @@ def test_tf_log_names_each_plan():
     assert r.returncode == 0 and "done" in r.stdout, r.stderr[-3000:]
     all_lines = [ln for ln in r.stderr.splitlines() if ln.startswith("[tilefuse] ")]
     lines = [ln for ln in all_lines if not ln.startswith("[tilefuse]   ")]
-    assert len(lines) == 7, r.stderr
+    assert len(lines) == 8, r.stderr
     assert "gemm256_kernel<4,1,f16> M=2048 K=4096 N=14336" in lines[0]
     assert "gemm256_kernel<4,1,f16> M=2048 K=14336 N=4096" in lines[1]
     assert "stream-K" in lines[1]
-    assert "gemm_ks_kernel<8," in lines[2] and "M=512" in lines[2]
+    assert "gemm_ks_kernel<8,1,f16,128>" in lines[2] and "M=512" in lines[2]
     assert "gemv_kernel<4,1," in lines[3] and "vector form" in lines[3]
     assert "gemv_kernel<4,16," in lines[4] and "matrix-core form" in lines[4]
     # 280 tiles of 256 x 256: one whole-tile round, the 24 after it on the K-split GEMM
     assert "gemm256_kernel<4,1,f16> M=1280 K=4096 N=14336" in lines[5]
     assert "K-split GEMM over the rest" in lines[5]
     rest = all_lines[all_lines.index(lines[5]) + 1]
-    assert "gemm_ks_kernel<4,1,f16>" in rest and "tiles 256..279" in rest and "192 tiles of 64x128" in rest
+    assert "gemm_ks_kernel<4,1,f16,128>" in rest and "tiles 256..279" in rest and "192 tiles of 64x128" in rest
     assert "gemv_kernel<8,8," in lines[6] and "128 panels x 2 column parts x 1 K slices" in lines[6]
+    assert "gemm_ks_kernel<4,1,f16,256> M=512" in lines[7] and "8x56 tiles of 64x256" in lines[7]
 
 
 def test_silent_without_tf_log():

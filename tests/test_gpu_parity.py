@@ -190,6 +190,9 @@ GEMM_SHAPES = [(4, 16, 2048, 2048, 128), (4, 17, 256, 136, 128), (4, 129, 512, 2
                # 192..256 tiles (ragged N with a clamped last panel; 9 and 5 chunks split
                # unevenly over the four waves; groups of 64 and 32), 4-bit with 65 rows
                (8, 384, 1152, 4088, 64), (8, 420, 640, 3968, 32), (4, 65, 4096, 776, 128),
+               # ... with 4-bit tiles of 64 x 256 (more than 1.5 rounds of 64 x 128 tiles): ragged
+               # rows, columns (the last tile partly past N) and K (31 chunks), groups of 32 and 64
+               (4, 1000, 3968, 4088, 32), (4, 300, 4096, 11008, 64), (4, 256, 4096, 14336, 128),
                # the 128-row GEMM: 4-bit beyond the 64 x 128 kernel's 1200 tiles, and
                # long K on few tiles (split-K)
                (4, 1000, 1024, 10000, 128), (4, 200, 12288, 520, 128), (8, 100, 16384, 264, 64),
@@ -211,7 +214,7 @@ def test_gemm_parity_small(tf, bits, M, K, N, G):
                                              ("gemm", 8, 5, 8192, 512), ("gemm", 4, 64, 4096, 1024),
                                              ("gemm", 8, 33, 4096, 520), ("gemm", 4, 300, 8192, 520),
                                              ("gemm", 8, 384, 512, 4096), ("gemm", 4, 200, 1024, 520),
-                                             ("gemm", 4, 1100, 512, 13304)])
+                                             ("gemm", 4, 1100, 512, 13304), ("gemm", 4, 512, 512, 14336)])
 def test_integer_invariant_bitexact(tf, kind, bits, M, K, N):
     """s = 1, z = 0, integer x in [-3, 3]: every partial sum is an integer below
     2^24, so the fp16 output must be RNE of the exact integer matmul."""
