@@ -97,6 +97,8 @@ def parse():
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the step, time every synthetic workload configuration "
                          "(one JSON line each)")
+    ap.add_argument("--rows", default=None,
+                    help="with --msweep: only these row counts (comma-separated, 1..8192)")
     ap.add_argument("--workload", default=None,
                     help="with --sweep: only this workload (a name of synth.WORKLOADS)")
     ap.add_argument("--dtype", default=None, choices=("f16", "bf16"),
@@ -442,12 +444,13 @@ def mlp_layers(torch, tf, Ms, dt, xall, p_gu, p_dn, H, I):
     torch.cuda.empty_cache()
 
 
-def msweep(torch, tf, make_inputs, target_ms=6.0):
+def msweep(torch, tf, make_inputs, target_ms=6.0, rows=None):
     """The paper's prompt-length sweep: W4A16 GEMM for M = 256..8192 (step
-    256) at (K, N) = (4096, 14336) and (14336, 4096).  Per shape one input
-    draw at M = 8192 (each M takes its first M rows of A) and enough copies of
-    the packed weight to stream it from HBM; HIP-graph replay as in --sweep,
-    with about `target_ms` of GPU time per graph."""
+    256, or the row counts in `rows`, each at most 8192) at (K, N) =
+    (4096, 14336) and (14336, 4096).  Per shape one input draw at M = 8192
+    (each M takes its first M rows of A) and enough copies of the packed
+    weight to stream it from HBM; HIP-graph replay as in --sweep, with about
+    `target_ms` of GPU time per graph."""
     from paper_2606_11357_amd.synth import M_SWEEP, M_SWEEP_SHAPES
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
@@ -459,7 +462,7 @@ def msweep(torch, tf, make_inputs, target_ms=6.0):
         copies = [p0] + [p0.clone() for _ in range(ncopy - 1)]
         xall = up(d["x"])
         del d
-        for M in M_SWEEP:
+        for M in (rows or M_SWEEP):
             x = xall[:M]
             y = torch.empty((M, N), dtype=torch.float16, device=dev)
             flops = 2.0 * M * N * K
@@ -515,7 +518,12 @@ def main():
         sweep(torch, tf, make_inputs, dtypes=dtypes, only=args.workload)
         return
     if args.msweep:
-        msweep(torch, tf, make_inputs)
+        rows = None
+        if args.rows:
+            rows = [int(r) for r in args.rows.split(",")]
+            if any(r < 1 or r > 8192 for r in rows):
+                sys.exit("--rows: row counts from 1 to 8192")
+        msweep(torch, tf, make_inputs, rows=rows)
         return
     if args.mlp:
         mlp(torch, tf, make_inputs, dtypes=dtypes)
