@@ -181,6 +181,7 @@ GEMM_CASES = [
     (4, 65, 1024, 1032, 128), (4, 300, 2048, 1024, 64), (4, 200, 1024, 1024, 32),
     (4, 777, 4096, 2056, 128),                                         # 64 x 128 GEMM, K over the waves
     (4, 1000, 3968, 4088, 32), (4, 512, 4096, 14336, 128),             # ... 64 x 256 tiles
+    (4, 300, 4096, 11008, 64),
     (4, 200, 12288, 264, 128), (4, 130, 480, 264, 96),                 # 128-row GEMM, generic kernel
     (4, 1024, 1024, 2048, 128), (4, 2048, 2048, 4096, 128), (4, 1100, 1024, 1000, 128),
     (4, 4096, 1024, 4096, 128),                                        # 256-row GEMM

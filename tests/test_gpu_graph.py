@@ -24,7 +24,8 @@ CASES = [("gemm", 4, 1100, 1024, 2320),   # 256-row tiles, stream-K
          ("gemm", 4, 40, 4096, 1024),     # streaming matrix-core form, 64 row slots
          ("gemm", 4, 20, 14336, 4096),    # streaming matrix-core form, factored, K split
          ("gemv", 4, 1, 14336, 4096),     # decode GEMV, K split
-         ("gemv", 8, 5, 4096, 520)]
+         ("gemv", 4, 1, 4096, 4096),      # decode GEMV, 4 column parts per panel
+         ("gemv", 8, 5, 4096, 520)]       # ... 2 column parts, ragged panels
 
 
 def _inputs(tf, dt, bits, M, K, N, seed):
