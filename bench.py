@@ -316,7 +316,15 @@ def graph_time_us(torch, fn, reps):
     return e0.elapsed_time(e1) * 1e3 / (3 * reps)
 
 
-def read_ceiling(torch, nbytes, reps=64):
+PROBE_SHAPES = ((224, 1024, 8), (224, 1024, 4), (256, 1024, 8), (256, 1024, 4), (256, 512, 16),
+                (512, 512, 8), (512, 1024, 4), (1024, 256, 8), (1024, 256, 16), (2048, 256, 4),
+                (2048, 256, 8), (4096, 256, 2))
+# the launch shapes that came out fastest for the decode GEMV's 30.5 MB
+# (profiles/context_references.md), timed beside every benchmark line
+PROBE_SHAPES_QUICK = ((224, 1024, 4), (4096, 256, 2), (2048, 256, 4))
+
+
+def read_ceiling(torch, nbytes, reps=64, shapes=PROBE_SHAPES):
     """Streaming-read ceiling for a launch that reads `nbytes` once: the read
     probe (paper_2606_11357_amd/probe, a kernel that only loads) over a sweep
     of launch shapes, rotating over enough buffers to exceed 512 MB so every
@@ -334,9 +342,7 @@ def read_ceiling(torch, nbytes, reps=64):
     bufs = [torch.ones(nbytes, device=dev, dtype=torch.uint8) for _ in range(ncopy)]
     sink = torch.zeros(4, device=dev, dtype=torch.int32)
     out = []
-    for grid, block, unroll in ((224, 1024, 8), (224, 1024, 4), (256, 1024, 8), (256, 1024, 4), (256, 512, 16),
-                                (512, 512, 8), (512, 1024, 4), (1024, 256, 8), (1024, 256, 16), (2048, 256, 4),
-                                (2048, 256, 8), (4096, 256, 2)):
+    for grid, block, unroll in shapes:
         def launch(i, g=grid, b=block, u=unroll):
             rc = lib.tf_probe_read(ctypes.c_void_p(bufs[i % ncopy].data_ptr()), nbytes, g, b, u,
                                    ctypes.c_void_p(sink.data_ptr()),
@@ -626,6 +632,17 @@ def main():
     gemv_us = gemv_ms * 1e3 / GEMV_REPS
     gemv_bytes = algo_bytes_w4(K1, N1)
     gemv_gbs = gemv_bytes / (gemv_us * 1e-6) / 1e9
+    # Context for the GEMV's fraction, measured after the timed region: the
+    # streaming-read ceiling for its byte count on this GPU (a kernel that
+    # only reads; the fastest of a few launch shapes).
+    try:
+        best = read_ceiling(torch, gemv_bytes, shapes=PROBE_SHAPES_QUICK)[0]
+        ceiling = {"value": best["read_GB/s"], "unit": "GB/s", "us_per_launch": best["us_per_launch"],
+                   "probe": "read-only kernel over the same byte count, grid %d x %d, %d loads in flight per "
+                            "thread" % (best["grid"], best["block"], best["unroll"]),
+                   "gemv_frac_of_ceiling": round(gemv_gbs / best["read_GB/s"], 4)}
+    except Exception as e:    # e.g. the probe library is not built: the line is printed regardless
+        ceiling = {"value": None, "reason": str(e)[:200]}
 
     line = {
         "metric": "W4A16 GEMM TFLOP/s (M=2048) + GEMV eff. HBM GB/s (M=1), % of roofline",
@@ -665,6 +682,7 @@ def main():
             "roofline": {"bound": "hbm", "achieved": round(gemv_gbs, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(gemv_gbs / PEAK_HBM_GBS, 4),
                          "traffic": recorded_traffic("tf_gemv.hip"), "kernel": "gemv_kernel"},
+            "read_ceiling": ceiling,
         },
         "gemm_ms_per_step": round(gemm_ms, 4),
         "gemm_us_per_shape": {f"K={K},N={N}": round(t * 1e3, 2) for (M, K, N), t in zip(GEMM_SHAPES, shape_ms)},
